@@ -1,0 +1,289 @@
+/*
+ * pulse.h -- C ABI of the MI355X (gfx950) sparse-KV decode hot path.
+ *
+ * One layer-step of I/O-centric sparse KV-cache offloading (PulseInfer,
+ * arXiv 2609.34555): score the current query against per-block key digests
+ * of one KV head, select one top-k block set shared by all KV heads
+ * (SoloHead, Sec. 4.4.1), take the set difference against the GPU-resident
+ * hot set, recall the missing blocks from pinned host DRAM into a GPU slot
+ * pool while updating the block table (Sec. 2.2, Sec. 4.4.2), and run sparse
+ * GQA decode attention over the selected blocks.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Ownership.  The caller owns every buffer.  The compute entry points never
+ *   allocate or free memory, never synchronise the host and keep no global
+ *   state; calls on disjoint buffers may run concurrently.
+ * Asynchrony.  Every compute call only enqueues work on `stream` and returns.
+ *   The return value reports errors detectable on the host before launch
+ *   (null pointers, unsupported shapes, workspace too small) and launch
+ *   failures (PULSE_ERR_HIP).  On any non-OK return nothing was enqueued.
+ * Device-detected errors.  Conditions that depend on device data (pool
+ *   exhaustion, a selection larger than k_max, an index outside its buffer)
+ *   are reported by writing the code into `*dev_status` (a device int32 that
+ *   the caller zeroes; the first error written wins, OK is never written).
+ *   Every such condition is checked before the memory access it guards, so a
+ *   bad index never turns into an out-of-bounds access.
+ * Element types.  K, V and queries are fp16 or bf16 (pulse_dtype); they are
+ *   passed as raw 16-bit element buffers.  Scores, outputs and LSE are fp32.
+ * Indices.  Block and slot indices are int32; block offsets are int64.
+ * Inputs must be finite.
+ *
+ * Supported shapes: head_dim 128; block_size 16, 32 or 64; num_q_heads a
+ * multiple of num_kv_heads with G = num_q_heads / num_kv_heads in [1, 16].
+ *
+ * KV block layout (host store and slot pool alike).  One block holds all KV
+ * heads of bs consecutive tokens, K first, then V:
+ *   K(h, t, c) at element ((0 * Hkv + h) * bs + t) * d + c      token-major
+ *   V(h, t, c) at element Hkv*bs*d + (h * d + c) * bs + t       channel-major
+ * so a block is U = 2 * Hkv * bs * d * 2 bytes (64 KiB at Hkv 8, bs 16).
+ * Tokens past the end of a context inside its last block must be zero.
+ * Requests are ragged: request r owns n_r = ceil(ctx_len[r] / bs) blocks,
+ * its global blocks are blk_off[r] .. blk_off[r+1]-1 (blk_off[0] = 0).
+ */
+#ifndef PULSE_H
+#define PULSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PULSE_API __attribute__((visibility("default")))
+
+typedef struct ihipStream_t* pulse_stream_t; /* a hipStream_t; NULL = default stream */
+
+typedef enum {
+    PULSE_OK = 0,
+    PULSE_ERR_INVALID_ARG = 1,     /* host-detected: null pointer, negative size, bad index arg */
+    PULSE_ERR_UNSUPPORTED = 2,     /* host-detected: shape or dtype outside the supported set */
+    PULSE_ERR_WORKSPACE = 3,       /* host-detected: ws_bytes below pulse_workspace_bytes() */
+    PULSE_ERR_POOL_EXHAUSTED = 4,  /* device-detected: more missing blocks than free slots */
+    PULSE_ERR_SELECT_OVERFLOW = 5, /* device-detected: forced + k_mid blocks exceed k_max */
+    PULSE_ERR_HIP = 6,             /* a HIP launch or runtime call failed */
+    PULSE_ERR_BAD_INDEX = 7        /* device-detected: block/slot index outside its buffer,
+                                      or a selection list not strictly ascending */
+} pulse_status;
+
+typedef enum { PULSE_F16 = 0, PULSE_BF16 = 1 } pulse_dtype;
+
+typedef struct {
+    int32_t num_q_heads;  /* Hq */
+    int32_t num_kv_heads; /* Hkv */
+    int32_t head_dim;     /* d, must be 128 */
+    int32_t block_size;   /* bs, tokens per KV block: 16, 32 or 64 */
+    int32_t dtype;        /* pulse_dtype of K, V and q */
+} pulse_shape;
+
+/* Device-resident statistics written by the recall (device memory). */
+typedef struct {
+    int32_t n_missing; /* blocks recalled (on pool exhaustion: blocks that would be) */
+    int32_t n_runs;    /* maximal runs of consecutive missing block indices */
+    int64_t bytes;     /* bytes copied host -> slot pool (0 on any device error) */
+} pulse_recall_stats;
+
+/* Human-readable name of a status code (static string). */
+PULSE_API const char* pulse_status_string(pulse_status s);
+
+/* Bytes of one KV block of `shape` (U above); 0 if the shape is unsupported. */
+PULSE_API size_t pulse_block_bytes(const pulse_shape* shape);
+
+/*
+ * Workspace bytes needed by every compute entry point for a batch of B
+ * requests, at most k_max selected blocks per request and total_blocks
+ * blocks in all (sum of n_r).  One workspace of this size serves any call
+ * with the same or smaller arguments, including pulse_decode_layer.
+ * Returns 0 for an unsupported shape or negative sizes.
+ */
+PULSE_API size_t pulse_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t k_max, int64_t total_blocks);
+
+/*
+ * a1. Per-block key digest of one KV head (Sec. 2.1: compact per-block
+ * digests in the style of Quest; Sec. 4.4.1: SoloHead keeps digests for one
+ * KV head per layer only).  For every block b of request r and channel c:
+ *   digests[b][0][c] = min over valid tokens t of K(kv_head, t, c)
+ *   digests[b][1][c] = max over valid tokens t of K(kv_head, t, c)
+ * exactly, in the KV dtype (-0 orders below +0).
+ *   kv           [total_blocks][block] elements; device memory or pinned,
+ *                host-mapped memory (the kernel reads it directly)
+ *   blk_off      device int64 [B+1];   ctx_len  device int32 [B]
+ *   total_blocks = blk_off[B] (host copy of the value, sizes the grid)
+ *   digests      device, [total_blocks][2][head_dim] elements, written
+ * Errors: host-detected only (a block whose request cannot be found is
+ * skipped and reported as PULSE_ERR_BAD_INDEX through dev_status if given;
+ * dev_status may be NULL).
+ */
+PULSE_API pulse_status pulse_build_digests(const pulse_shape* shape, const void* kv, const int64_t* blk_off,
+                                 const int32_t* ctx_len, int32_t B, int64_t total_blocks,
+                                 int32_t kv_head, void* digests, int32_t* dev_status,
+                                 pulse_stream_t stream);
+
+/*
+ * a2 + a3. SoloHead top-k block selection (Sec. 4.4.1; budget split into
+ * sink, local and middle tokens, Sec. 5 setup; sink and local blocks stay
+ * resident, Sec. 4.2).  For request r with n_r blocks:
+ *   score[b] = (1/G) * sum_{g<G} sum_c max(q[r][h*G+g][c] * mn[b][c],
+ *                                          q[r][h*G+g][c] * mx[b][c])
+ *   with h = solo_kv_head, computed in fp32;
+ *   forced  = blocks j < n_sink_blocks and j >= n_r - n_local_blocks;
+ *   middle  = the other blocks; k' = min(max(k_mid[r], 0), #middle);
+ *   chosen  = the k' middle blocks of highest score, equal scores taken in
+ *             ascending block order;
+ *   sel_idx[r][0 .. sel_cnt[r]) = forced U chosen, ascending; the rest -1.
+ *   q            device [B][Hq][d] elements
+ *   digests      device [total_blocks][2][d] elements of solo_kv_head
+ *   k_mid        device int32 [B] middle-block budget per request
+ *   sel_idx      device int32 [B][k_max], written;  sel_cnt device int32 [B]
+ *   scores       optional device float [total_blocks]: if non-NULL receives
+ *                the scores of middle blocks (forced entries are left as is)
+ * A request whose selection would exceed k_max gets sel_cnt = 0 and
+ * PULSE_ERR_SELECT_OVERFLOW in *dev_status (dev_status must be non-NULL).
+ */
+PULSE_API pulse_status pulse_select_solohead(const pulse_shape* shape, const void* q, const void* digests,
+                                   const int64_t* blk_off, int32_t B, int64_t total_blocks,
+                                   int32_t solo_kv_head, const int32_t* k_mid, int32_t n_sink_blocks,
+                                   int32_t n_local_blocks, int32_t k_max, int32_t* sel_idx,
+                                   int32_t* sel_cnt, float* scores, int32_t* dev_status, void* ws,
+                                   size_t ws_bytes, pulse_stream_t stream);
+
+/*
+ * a4 + a5 + a6. Set difference, slot allocation and gather-scatter recall
+ * (Sec. 2.2: B_recall = B_topk minus B_gpu, then copy from DRAM; Sec. 4.4.2:
+ * scattered blocks move as coalesced transfers and land in the KV cache).
+ *   missing = [(r, j) : r ascending, j = sel_idx[r][i] in listed order,
+ *              block_table[r][j] == -1]
+ *   the g-th missing block takes slot s = free_slots[*free_head + g];
+ *   block_table[r][j] = s; slot_pool[s] = host_kv[blk_off[r] + j] (U bytes);
+ *   *free_head += #missing; stats = {#missing, #runs, #missing * U}.
+ * A run is a maximal stretch of listed missing blocks of one request whose
+ * indices increase by one; runs are read from host memory as contiguous
+ * streams.  The copy is done by GPU loads of the pinned host memory.
+ *   host_kv      pinned, host-mapped [total_blocks][block] (hipHostMalloc
+ *                with hipHostMallocMapped); read only
+ *   sel_idx/sel_cnt  as produced by pulse_select_solohead (strictly
+ *                ascending per request)
+ *   block_table  device int32 [B][max_blocks], -1 = not resident; updated
+ *   free_slots   device int32 [n_free];  free_head device int32, updated
+ *   slot_pool    device [n_slots][block] elements; free slots are written
+ *   stats        device pulse_recall_stats, written
+ *   dev_status   device int32, required
+ * If #missing > n_free - *free_head, PULSE_ERR_POOL_EXHAUSTED is reported and
+ * the table, pool and free_head are left unchanged; likewise for any index
+ * outside its buffer (PULSE_ERR_BAD_INDEX).
+ */
+PULSE_API pulse_status pulse_recall_gather(const pulse_shape* shape, const void* host_kv, const int64_t* blk_off,
+                                 int32_t B, const int32_t* sel_idx, const int32_t* sel_cnt, int32_t k_max,
+                                 int32_t* block_table, int32_t max_blocks, const int32_t* free_slots,
+                                 int32_t* free_head, int32_t n_free, void* slot_pool, int32_t n_slots,
+                                 pulse_recall_stats* stats, int32_t* dev_status, void* ws,
+                                 size_t ws_bytes, pulse_stream_t stream);
+
+/*
+ * a7. Sparse GQA decode attention over the selected blocks (the attention
+ * that follows recall, Sec. 2.2 and Sec. 4.2.1).  For request r and query
+ * head hq, KV head h = hq / G:
+ *   logit_t = sm_scale * q[r][hq] . K(h, t)   over the valid tokens t of the
+ *             blocks sel_idx[r][0 .. sel_cnt[r]), read from
+ *             slot_pool[block_table[r][j]]
+ *   out[r][hq] = sum_t softmax(logit)_t V(h, t)      (fp32)
+ *   lse[r][hq] = log sum_t exp(logit_t)              (fp32, optional)
+ * An empty selection gives out = 0 and lse = -inf.  Products and sums are
+ * accumulated in fp32.
+ *   out          device float [B][Hq][d];  lse optional device float [B][Hq]
+ *   dev_status   device int32, required (unresident block -> BAD_INDEX)
+ */
+PULSE_API pulse_status pulse_sparse_decode_attn(const pulse_shape* shape, const void* q, const void* slot_pool,
+                                      int32_t n_slots, const int32_t* block_table, int32_t max_blocks,
+                                      const int32_t* sel_idx, const int32_t* sel_cnt, int32_t k_max,
+                                      const int32_t* ctx_len, int32_t B, float sm_scale, float* out,
+                                      float* lse, int32_t* dev_status, void* ws, size_t ws_bytes,
+                                      pulse_stream_t stream);
+
+/* All arguments of one layer-step (pulse_decode_layer).  Field meanings are
+ * those of the entry points above. */
+typedef struct {
+    pulse_shape shape;
+    int32_t B;
+    int64_t total_blocks;
+    const int32_t* ctx_len;   /* device [B] */
+    const int64_t* blk_off;   /* device [B+1] */
+    const void* q;            /* device [B][Hq][d] */
+    const void* digests;      /* device [total_blocks][2][d] of solo_kv_head */
+    int32_t solo_kv_head;
+    const int32_t* k_mid;     /* device [B] */
+    int32_t n_sink_blocks;
+    int32_t n_local_blocks;
+    int32_t k_max;
+    int32_t* sel_idx;         /* device [B][k_max], written */
+    int32_t* sel_cnt;         /* device [B], written */
+    const void* host_kv;      /* pinned host-mapped store */
+    int32_t* block_table;     /* device [B][max_blocks], updated */
+    int32_t max_blocks;
+    const int32_t* free_slots;/* device [n_free] */
+    int32_t* free_head;       /* device, updated */
+    int32_t n_free;
+    void* slot_pool;          /* device [n_slots][block] */
+    int32_t n_slots;
+    pulse_recall_stats* stats;/* device, written */
+    float sm_scale;
+    float* out;               /* device [B][Hq][d] */
+    float* lse;               /* device [B][Hq] or NULL */
+    int32_t* dev_status;      /* device, required */
+    void* ws;
+    size_t ws_bytes;
+    void* const* events;      /* optional host array of 5 hipEvent_t, recorded on the
+                                 stream before score, select, recall copy, attention and
+                                 after attention (stage timing); NULL = none */
+} pulse_layer_args;
+
+/*
+ * a8. One decode layer-step: score + select (with the set difference folded
+ * into the selection pass), allocation + recall, attention, all enqueued on
+ * one stream with no host synchronisation (zero-sync submission, Sec. 4.5).
+ * Results are those of the four calls above made in order.
+ */
+PULSE_API pulse_status pulse_decode_layer(const pulse_layer_args* args, pulse_stream_t stream);
+
+/* ---- measurement helpers (host side; not part of the compute path) ---- */
+
+/*
+ * Pinned host memory for the KV store: hipHostMalloc with hipHostMallocMapped
+ * | hipHostMallocPortable, plus hipHostMallocCoherent when `coherent` is
+ * non-zero (fine-grained) or hipHostMallocNonCoherent otherwise.  *host_ptr
+ * is usable by CPU code and by GPU kernels.  Free with pulse_host_free.
+ */
+PULSE_API pulse_status pulse_host_alloc(size_t bytes, int32_t coherent, void** host_ptr);
+PULSE_API pulse_status pulse_host_free(void* host_ptr);
+
+/*
+ * Per-block hipMemcpyAsync recall baseline (one DMA per unit, as the
+ * threaded per-block copy that the paper's gather-scatter engine is compared
+ * with, Sec. 4.4.2).  Copies n units of unit_bytes from
+ * host_kv + src_units[i] * unit_bytes to pool + dst_units[i] * unit_bytes.
+ * src_units / dst_units are HOST arrays.  Enqueued on `stream`.
+ */
+PULSE_API pulse_status pulse_baseline_memcpy_units(const void* host_kv, void* pool, const int64_t* src_units,
+                                         const int64_t* dst_units, int32_t n, size_t unit_bytes,
+                                         pulse_stream_t stream);
+
+/*
+ * Host-link probe: a streaming kernel that copies `bytes` (a multiple of
+ * 16384) from pinned host memory to device memory with the load pattern of
+ * the recall kernel.  Used to measure the link's achievable read bandwidth.
+ */
+PULSE_API pulse_status pulse_probe_host_read(const void* host_src, void* dev_dst, size_t bytes, pulse_stream_t stream);
+
+/* Timing events for pulse_layer_args.events: n hipEvent_t handles written to
+ * events[0..n); destroy with pulse_events_destroy. */
+PULSE_API pulse_status pulse_events_create(int32_t n, void** events);
+PULSE_API pulse_status pulse_events_destroy(int32_t n, void* const* events);
+/* Milliseconds between two completed events (hipEventElapsedTime). */
+PULSE_API pulse_status pulse_event_elapsed_ms(void* start, void* stop, float* ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PULSE_H */

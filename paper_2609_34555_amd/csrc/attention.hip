@@ -1,0 +1,314 @@
+// attention.hip -- split-K sparse GQA decode attention over the selected
+// blocks of the slot pool, for gfx950 (the attention that follows recall,
+// Sec. 2.2 and Sec. 4.2.1).
+//
+// One wavefront owns (request r, KV head h, split s): a contiguous range of
+// the request's selected blocks.  The G query heads of h share every K/V
+// byte the wave reads, so the contraction is a batched GQA tile:
+//   S^T[32 tokens x 16] = K[32 x 128] . Q^T[128 x 16]   (G <= 16 query columns)
+//   O[16 x 128]        += P[16 x 32]  . V[32 x 128]
+// both on v_mfma_f32_16x16x32_{bf16,f16}.  Each lane's MFMA operands are 16
+// contiguous bytes in HBM: K is stored token-major and V channel-major, so
+// neither operand needs an LDS transpose.  The S^T tile rows are assigned
+// to tokens so that its accumulator layout is exactly the P operand layout
+// of the P.V product (lane = query column, 8 consecutive tokens per lane
+// group), so softmax probabilities never leave registers.
+//
+// Precision: K, V, q are consumed as stored (products exact in fp32, fp32
+// accumulation).  P is split into hi + lo 16-bit parts (two MFMAs), which
+// keeps the P.V product at ~2^-16 relative error instead of the 2^-9 of a
+// single bf16 rounding.  Softmax is online per 32-token step in the log2
+// domain.  Partials (m, l, O) per split go to the workspace; a combine
+// kernel merges them into fp32 out and LSE.
+#include "pulse_internal.h"
+
+namespace pulse {
+
+template <int DT>
+struct Mfma;
+template <>
+struct Mfma<PULSE_BF16> {
+    typedef bf16x8 vec;
+    typedef __bf16 elem;
+    __device__ static inline f32x4 mac(vec a, vec b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline void split(float p, __bf16& hi, __bf16& lo) {
+        hi = (__bf16)p;
+        lo = (__bf16)(p - (float)hi);
+    }
+};
+template <>
+struct Mfma<PULSE_F16> {
+    typedef f16x8 vec;
+    typedef _Float16 elem;
+    __device__ static inline f32x4 mac(vec a, vec b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline void split(float p, _Float16& hi, _Float16& lo) {
+        hi = (_Float16)p;
+        lo = (_Float16)(p - (float)hi);
+    }
+};
+
+template <int DT>
+__device__ inline typename Mfma<DT>::vec load_vec(const uint16_t* p) {
+    return __builtin_bit_cast(typename Mfma<DT>::vec, *reinterpret_cast<const u32x4*>(p));
+}
+template <int DT>
+__device__ inline typename Mfma<DT>::vec zero_vec() {
+    return __builtin_bit_cast(typename Mfma<DT>::vec, u32x4{0, 0, 0, 0});
+}
+
+template <int DT, int BS>
+__global__ __launch_bounds__(64) void attn_splitk_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ pool, int32_t n_slots,
+    const int32_t* __restrict__ table, int32_t max_blocks, const int32_t* __restrict__ sel_idx,
+    const int32_t* __restrict__ sel_cnt, int32_t k_max, const int32_t* __restrict__ ctx_len, int32_t Hq,
+    int32_t Hkv, int32_t G, int32_t eps, int32_t n_split, float scale_log2, float* __restrict__ ws_o,
+    float2* __restrict__ ws_ml, int32_t* status) {
+    using M = Mfma<DT>;
+    using vec = typename M::vec;
+    const int lane = threadIdx.x;
+    const int col = lane & 15;  // MFMA column: query head (QK^T), channel (PV)
+    const int grp = lane >> 4;  // lane group: 8-channel / 8-token slice
+    const int s = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+    const size_t unit = ((size_t)r * Hkv + h) * n_split + s;
+
+    int32_t cnt = sel_cnt[r];
+    if (cnt < 0 || cnt > k_max) {
+        if (lane == 0) report(status, PULSE_ERR_BAD_INDEX);
+        cnt = 0;
+    }
+    const int e0 = s * eps;
+    const int ne = min(e0 + eps, cnt) - e0;  // entries of this split
+    if (ne <= 0) {
+        if (lane < G) ws_ml[unit * G + lane] = make_float2(-INFINITY, 0.f);
+        return;
+    }
+    // entry metadata, one entry per lane (eps <= 64)
+    const int ctx = ctx_len[r];
+    const int64_t n_r = ((int64_t)ctx + BS - 1) / BS;
+    int my_slot = -1, my_nv = 0;
+    if (lane < ne) {
+        const int32_t j = sel_idx[(size_t)r * k_max + e0 + lane];
+        if (j >= 0 && j < n_r && j < max_blocks) {
+            const int32_t sl = table[(size_t)r * max_blocks + j];
+            if (sl >= 0 && sl < n_slots) {
+                my_slot = sl;
+                const int64_t v = (int64_t)ctx - (int64_t)j * BS;
+                my_nv = v >= BS ? BS : (int)v;
+            }
+        }
+        if (my_slot < 0) report(status, PULSE_ERR_BAD_INDEX);
+    }
+    // Q^T operand: lane holds q[g = col][8 channels of slice grp + 32 kc]
+    vec qb[4];
+    {
+        const uint16_t* qr = q + ((size_t)r * Hq + (size_t)h * G + col) * kHeadDim + grp * 8;
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) qb[kc] = col < G ? load_vec<DT>(qr + 32 * kc) : zero_vec<DT>();
+    }
+    const size_t E = (size_t)2 * Hkv * BS * kHeadDim;
+    const size_t k_head = (size_t)h * BS * kHeadDim;
+    const size_t v_head = (size_t)Hkv * BS * kHeadDim + (size_t)h * kHeadDim * BS;
+
+    f32x4 acc[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+    const int tokens = ne * BS;
+
+    for (int t0 = 0; t0 < tokens; t0 += kChunkTokens) {
+        // --- K operand: MFMA row m = col maps to token 8*(col/4) + 4*sub + col%4
+        const int ka_seq = t0 + 8 * (col >> 2);
+        const int ka_e = ka_seq / BS;
+        const int ka_slot = __shfl(my_slot, ka_e < ne ? ka_e : 0);
+        const int ka_nv = __shfl(my_nv, ka_e < ne ? ka_e : 0);
+        vec ka[2][4];
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub) {
+            const int row = ka_seq % BS + 4 * sub + (col & 3);
+            const bool ok = ka_e < ne && ka_slot >= 0 && row < ka_nv;
+            const uint16_t* kp = pool + (size_t)(ok ? ka_slot : 0) * E + k_head + (size_t)row * kHeadDim + grp * 8;
+#pragma unroll
+            for (int kc = 0; kc < 4; ++kc) ka[sub][kc] = ok ? load_vec<DT>(kp + 32 * kc) : zero_vec<DT>();
+        }
+        // --- V operand: lane group grp holds tokens 8*grp .. 8*grp+7 of channel col + 16*tile
+        const int pv_seq = t0 + 8 * grp;
+        const int pv_e = pv_seq / BS;
+        const int pv_slot = __shfl(my_slot, pv_e < ne ? pv_e : 0);
+        const int pv_nv = __shfl(my_nv, pv_e < ne ? pv_e : 0);
+        const int pv_row = pv_seq % BS;
+        const bool pv_ok = pv_e < ne && pv_slot >= 0;
+        vec vb[8];
+        {
+            const uint16_t* vp = pool + (size_t)(pv_ok ? pv_slot : 0) * E + v_head + (size_t)col * BS + pv_row;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) vb[t] = pv_ok ? load_vec<DT>(vp + (size_t)16 * t * BS) : zero_vec<DT>();
+        }
+        // --- S^T = K . Q^T
+        f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) {
+            s1 = M::mac(ka[0][kc], qb[kc], s1);
+            s2 = M::mac(ka[1][kc], qb[kc], s2);
+        }
+        // lane (col, grp) now holds query col, tokens pv_seq + 0..7
+        float x[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] = s1[i] * scale_log2;
+            x[4 + i] = s2[i] * scale_log2;
+        }
+        float cm = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            if (!pv_ok || pv_row + i >= pv_nv) x[i] = -INFINITY;
+            cm = fmaxf(cm, x[i]);
+        }
+        cm = fmaxf(cm, __shfl_xor(cm, 16));
+        cm = fmaxf(cm, __shfl_xor(cm, 32));
+        const float m_new = fmaxf(m_run, cm);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(m_run - m_use);
+        float psum = 0.f;
+        vec ph, pl;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float p = exp2f(x[i] - m_use);
+            psum += p;
+            typename M::elem hi, lo;
+            M::split(p, hi, lo);
+            ph[i] = hi;
+            pl[i] = lo;
+        }
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+        // rescale accumulator rows g' = 4*grp + v by alpha of query g'
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float av = __shfl(alpha, 4 * grp + v);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc[t][v] *= av;
+        }
+        // --- O += P . V  (hi and lo parts of P)
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            acc[t] = M::mac(ph, vb[t], acc[t]);
+            acc[t] = M::mac(pl, vb[t], acc[t]);
+        }
+    }
+    l_run += __shfl_xor(l_run, 16);
+    l_run += __shfl_xor(l_run, 32);
+    if (grp == 0 && col < G) ws_ml[unit * G + col] = make_float2(m_run, l_run);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        const int g = 4 * grp + v;
+        if (g < G) {
+            float* o = ws_o + (unit * G + g) * kHeadDim + col;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) o[16 * t] = acc[t][v];
+        }
+    }
+}
+
+// one wavefront per (request, query head); lane owns channels 2*lane, 2*lane+1
+__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ ws_o,
+                                                           const float2* __restrict__ ws_ml,
+                                                           const int32_t* __restrict__ sel_cnt, int32_t k_max,
+                                                           int32_t B, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps,
+                                                           int32_t n_split, float* __restrict__ out,
+                                                           float* __restrict__ lse) {
+    const int lane = threadIdx.x & 63;
+    const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (item >= (int64_t)B * Hq) return;
+    const int r = (int)(item / Hq), hq = (int)(item % Hq);
+    const int h = hq / G, g = hq % G;
+    int32_t cnt = sel_cnt[r];
+    cnt = cnt < 0 ? 0 : (cnt > k_max ? k_max : cnt);
+    const int ns = (cnt + eps - 1) / eps;
+    const size_t u0 = ((size_t)r * Hkv + h) * n_split;
+    float M = -INFINITY;
+    for (int s = 0; s < ns; ++s) M = fmaxf(M, ws_ml[(u0 + s) * G + g].x);
+    float2* o2 = reinterpret_cast<float2*>(out + item * kHeadDim);
+    if (M == -INFINITY) {
+        o2[lane] = make_float2(0.f, 0.f);
+        if (lse && lane == 0) lse[item] = -INFINITY;
+        return;
+    }
+    float L = 0.f, a0 = 0.f, a1 = 0.f;
+    for (int s = 0; s < ns; ++s) {
+        const float2 ml = ws_ml[(u0 + s) * G + g];
+        if (ml.x == -INFINITY) continue;
+        const float w = exp2f(ml.x - M);
+        L += ml.y * w;
+        const float2 o = reinterpret_cast<const float2*>(ws_o + ((u0 + s) * G + g) * kHeadDim)[lane];
+        a0 += o.x * w;
+        a1 += o.y * w;
+    }
+    o2[lane] = make_float2(a0 / L, a1 / L);
+    if (lse && lane == 0) lse[item] = (M + log2f(L)) * 0.69314718055994531f;
+}
+
+AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
+    // entries per 32-token step; a split covers >= 2 steps, <= 64 entries
+    const int32_t step = bs >= kChunkTokens ? 1 : kChunkTokens / bs;
+    const int64_t units = (int64_t)B * Hkv;
+    const int64_t target_waves = 4096;
+    int64_t want = units > 0 ? (target_waves + units - 1) / units : 1;
+    int64_t min_entries = (bs >= 2 * kChunkTokens) ? 1 : (2 * kChunkTokens) / bs;
+    int64_t max_split = (k_max + min_entries - 1) / min_entries;
+    if (want > max_split) want = max_split;
+    if (want < 1) want = 1;
+    int64_t eps = (k_max + want - 1) / want;
+    eps = ((eps + step - 1) / step) * step;
+    if (eps > 64) eps = 64;
+    if (eps < 1) eps = 1;
+    AttnPlan p;
+    p.entries_per_split = (int32_t)eps;
+    p.n_split = (int32_t)((k_max + eps - 1) / eps);
+    return p;
+}
+
+template <int DT, int BS>
+static void launch_attn_t(dim3 grid, hipStream_t st, const void* q, const void* pool, int32_t n_slots,
+                          const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
+                          int32_t k_max, const int32_t* ctx_len, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps,
+                          int32_t n_split, float scale_log2, float* ws_o, float2* ws_ml, int32_t* status) {
+    hipLaunchKernelGGL((attn_splitk_kernel<DT, BS>), grid, dim3(64), 0, st, (const uint16_t*)q,
+                       (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, Hkv,
+                       G, eps, n_split, scale_log2, ws_o, ws_ml, status);
+}
+
+hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
+                            const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
+                            int32_t k_max, const int32_t* ctx_len, int32_t B, float sm_scale, float* out, float* lse,
+                            float* ws_o, float2* ws_ml, int32_t* status, hipStream_t st) {
+    if (B == 0) return hipSuccess;
+    const int32_t Hkv = s.num_kv_heads, Hq = s.num_q_heads, G = Hq / Hkv;
+    const AttnPlan p = attn_plan(B, Hkv, k_max, s.block_size);
+    dim3 grid((unsigned)p.n_split, (unsigned)Hkv, (unsigned)B);
+    const float scale_log2 = sm_scale * 1.4426950408889634f;
+#define PULSE_ATTN(DT, BS)                                                                                         \
+    launch_attn_t<DT, BS>(grid, st, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, Hkv, \
+                          G, p.entries_per_split, p.n_split, scale_log2, ws_o, ws_ml, status)
+    if (s.dtype == PULSE_BF16) {
+        if (s.block_size == 16) PULSE_ATTN(PULSE_BF16, 16);
+        else if (s.block_size == 32) PULSE_ATTN(PULSE_BF16, 32);
+        else PULSE_ATTN(PULSE_BF16, 64);
+    } else {
+        if (s.block_size == 16) PULSE_ATTN(PULSE_F16, 16);
+        else if (s.block_size == 32) PULSE_ATTN(PULSE_F16, 32);
+        else PULSE_ATTN(PULSE_F16, 64);
+    }
+#undef PULSE_ATTN
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t items = (int64_t)B * Hq;
+    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, ws_o, ws_ml, sel_cnt,
+                       k_max, B, Hq, Hkv, G, p.entries_per_split, p.n_split, out, lse);
+    return hipGetLastError();
+}
+
+}  // namespace pulse

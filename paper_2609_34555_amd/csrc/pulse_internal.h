@@ -1,0 +1,126 @@
+// pulse_internal.h -- types, element helpers, workspace layout and launch
+// declarations shared by the gfx950 kernels of the sparse-KV decode path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/pulse.h"
+
+namespace pulse {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
+
+constexpr int kHeadDim = 128;
+constexpr int kWave = 64;
+constexpr int kMaxGroup = 16;   // G = Hq / Hkv padded to one 16-wide MFMA tile
+constexpr int kChunkTokens = 32;  // attention processes 32 tokens per MFMA step
+
+// ---- device status --------------------------------------------------------
+
+__device__ inline void report(int32_t* status, int32_t code) {
+    if (status) atomicCAS(status, 0, code);
+}
+
+// ---- 16-bit element helpers ------------------------------------------------
+
+// Order-preserving map of a sign-magnitude 16-bit float pattern onto uint16:
+// increasing values give increasing keys, and -0 sorts just below +0.
+__device__ inline uint32_t key16(uint32_t x) { return (x & 0x8000u) ? (~x & 0xFFFFu) : (x | 0x8000u); }
+__device__ inline uint32_t unkey16(uint32_t k) { return (k & 0x8000u) ? (k & 0x7FFFu) : (~k & 0xFFFFu); }
+
+// Order-preserving map of fp32 onto uint32 (both zeros map to the key of +0).
+__device__ inline uint32_t key32(float s) {
+    s = s + 0.0f;  // -0 -> +0
+    uint32_t u = __float_as_uint(s);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+template <int DT>
+__device__ inline float elem_to_float(uint16_t x);
+template <>
+__device__ inline float elem_to_float<PULSE_BF16>(uint16_t x) { return __uint_as_float((uint32_t)x << 16); }
+template <>
+__device__ inline float elem_to_float<PULSE_F16>(uint16_t x) {
+    _Float16 h;
+    __builtin_memcpy(&h, &x, 2);
+    return (float)h;
+}
+
+// ---- workspace layout -----------------------------------------------------
+
+struct AttnPlan {
+    int32_t entries_per_split;  // selected blocks handled by one wave
+    int32_t n_split;            // splits per (request, KV head)
+};
+
+struct WsLayout {
+    size_t scores;     // float [total_blocks]
+    size_t miss_list;  // int32 [B][k_max]   missing block indices, listed order
+    size_t miss_cnt;   // int32 [B]
+    size_t run_cnt;    // int32 [B]
+    size_t req_err;    // int32 [B]          per-request plan error (0 = ok)
+    size_t misc;       // int32 [16]         [0] = free_head snapshot
+    size_t attn_o;     // float [B][Hkv][max_split][G][d]
+    size_t attn_ml;    // float2 [B][Hkv][max_split][G]
+    size_t total;
+};
+
+// Maximum number of splits any call with these arguments may use.
+inline int32_t attn_max_split(int32_t k_max, int32_t bs) {
+    int64_t chunks = ((int64_t)k_max * bs + kChunkTokens - 1) / kChunkTokens;
+    return (int32_t)(chunks < 1 ? 1 : chunks);
+}
+
+AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs);
+WsLayout ws_layout(const pulse_shape& s, int32_t B, int32_t k_max, int64_t total_blocks);
+bool shape_supported(const pulse_shape* s);
+
+// ---- launchers (each returns hipSuccess or the launch error) --------------
+
+hipError_t launch_build_digests(const pulse_shape& s, const void* kv, const int64_t* blk_off,
+                                const int32_t* ctx_len, int32_t B, int64_t total_blocks, int32_t kv_head,
+                                void* digests, int32_t* status, hipStream_t st);
+
+hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
+                        int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
+                        float* scores, hipStream_t st);
+
+// select (a3); when table != nullptr the set difference (a4) is folded in and
+// the recall plan (miss list, counts, runs, free_head snapshot) is written.
+hipError_t launch_select(const int64_t* blk_off, int32_t B, const float* scores, const int32_t* k_mid,
+                         int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* sel_idx,
+                         int32_t* sel_cnt, const int32_t* table, int32_t max_blocks, int32_t n_slots,
+                         const int32_t* free_head, int32_t* miss_list, int32_t* miss_cnt,
+                         int32_t* run_cnt, int32_t* req_err, int32_t* misc, int32_t* status,
+                         hipStream_t st);
+
+hipError_t launch_recall_plan(const int64_t* blk_off, int32_t B, const int32_t* sel_idx,
+                              const int32_t* sel_cnt, int32_t k_max, const int32_t* table,
+                              int32_t max_blocks, int32_t n_slots, const int32_t* free_head,
+                              int32_t* miss_list, int32_t* miss_cnt, int32_t* run_cnt, int32_t* req_err,
+                              int32_t* misc, int32_t* status, hipStream_t st);
+
+hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32_t B, int32_t k_max,
+                              int32_t* table, int32_t max_blocks, const int32_t* free_slots,
+                              int32_t* free_head, int32_t n_free, void* pool, int32_t n_slots,
+                              size_t unit_bytes, const int32_t* miss_list, const int32_t* miss_cnt,
+                              const int32_t* run_cnt, const int32_t* req_err, const int32_t* misc,
+                              pulse_recall_stats* stats, int32_t* status, hipStream_t st);
+
+hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
+                            const int32_t* table, int32_t max_blocks, const int32_t* sel_idx,
+                            const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t B,
+                            float sm_scale, float* out, float* lse, float* ws_o, float2* ws_ml,
+                            int32_t* status, hipStream_t st);
+
+hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
+
+}  // namespace pulse

@@ -1,0 +1,223 @@
+// recall.hip -- set difference, slot allocation and the gather-scatter
+// recall of missing KV blocks from pinned host DRAM into the GPU slot pool.
+//
+// Sec. 2.2: after selection, B_recall = B_topk minus B_gpu is copied from
+// DRAM to the GPU.  Sec. 4.4.2: scattered blocks should cross the host link
+// as large coalesced transfers and land in the GPU KV cache.  Here the GPU
+// itself gathers: wavefronts issue 16-byte non-temporal loads straight from
+// the pinned, host-mapped store (the host->device crossing happens inside
+// the load instructions) and store into the slots taken from the free list.
+// Missing blocks are processed in (request, block) order, so every run of
+// consecutive missing blocks is read as one contiguous host stream spread
+// over consecutive workgroups.
+//
+// Plan kernel (one workgroup per request): set difference of the selection
+// against the block table -> listed missing blocks, count, runs.
+// Copy kernel (persistent grid): every workgroup scans the per-request
+// counts (small), checks the pool capacity, then copies 4 KiB * LPT chunks;
+// the chunk that starts a block also writes its block-table entry.
+#include "pulse_internal.h"
+
+namespace pulse {
+
+constexpr int kPlanThreads = 256;
+constexpr int kCopyThreads = 256;
+constexpr int kMaxBatch = 4096;  // requests per call supported by the copy kernel
+
+__device__ inline uint64_t lanemask_lt_r() {
+    const int lane = threadIdx.x & 63;
+    return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+}
+
+__global__ __launch_bounds__(kPlanThreads) void recall_plan_kernel(
+    const int64_t* __restrict__ blk_off, const int32_t* __restrict__ sel_idx, const int32_t* __restrict__ sel_cnt,
+    int32_t k_max, const int32_t* __restrict__ table, int32_t max_blocks, int32_t n_slots,
+    const int32_t* __restrict__ free_head, int32_t* __restrict__ miss_list, int32_t* __restrict__ miss_cnt,
+    int32_t* __restrict__ run_cnt, int32_t* __restrict__ req_err, int32_t* __restrict__ misc, int32_t* status) {
+    __shared__ uint32_t wc[kPlanThreads / kWave][2];
+    __shared__ int32_t sh_err;
+    const int r = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    if (r == 0 && tid == 0) misc[0] = *free_head;
+    if (tid == 0) sh_err = 0;
+    __syncthreads();
+    const int64_t n = blk_off[r + 1] - blk_off[r];
+    int32_t cnt = sel_cnt[r];
+    int32_t my_err = 0;
+    if (cnt < 0 || cnt > k_max) {
+        my_err = PULSE_ERR_BAD_INDEX;
+        cnt = 0;
+    }
+    const int32_t* row = sel_idx + (size_t)r * k_max;
+    const int32_t* trow = table + (size_t)r * max_blocks;
+    uint32_t carry = 0, runs = 0;
+    for (int32_t tile = 0; tile < cnt; tile += kPlanThreads) {
+        const int32_t i = tile + tid;
+        const bool in = i < cnt;
+        int32_t j = in ? row[i] : 0;
+        const int32_t pj = (in && i > 0) ? row[i - 1] : -1;
+        bool bad = in && (j < 0 || j >= n || j >= max_blocks || (i > 0 && j <= pj));
+        bool miss = false, prev_miss = false;
+        if (in && !bad) {
+            const int32_t v = trow[j];
+            if (v >= n_slots) bad = true;
+            else miss = v < 0;
+            // the previous listed entry continues the run iff it is block j-1 and missing
+            if (i > 0 && pj == j - 1) prev_miss = trow[pj] < 0;
+        }
+        if (bad) my_err = PULSE_ERR_BAD_INDEX;
+        const bool start = miss && !prev_miss;
+        const uint64_t m_miss = __ballot(miss);
+        const uint64_t m_start = __ballot(start);
+        if (lane == 0) { wc[wid][0] = (uint32_t)__popcll(m_miss); wc[wid][1] = (uint32_t)__popcll(m_start); }
+        __syncthreads();
+        uint32_t pos = carry + (uint32_t)__popcll(m_miss & lanemask_lt_r()), tm = 0, ts = 0;
+        for (int w = 0; w < kPlanThreads / kWave; ++w) {
+            if (w < wid) pos += wc[w][0];
+            tm += wc[w][0];
+            ts += wc[w][1];
+        }
+        if (miss && pos < (uint32_t)k_max) miss_list[(size_t)r * k_max + pos] = j;
+        carry += tm;
+        runs += ts;
+        __syncthreads();
+    }
+    if (my_err) atomicCAS(&sh_err, 0, my_err);
+    __syncthreads();
+    if (tid == 0) {
+        miss_cnt[r] = (int32_t)carry;
+        run_cnt[r] = (int32_t)runs;
+        req_err[r] = sh_err;
+        if (sh_err) report(status, sh_err);
+    }
+}
+
+template <int LPT>
+__device__ inline void copy_chunk(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, int tid) {
+    u32x4 v[LPT];
+#pragma unroll
+    for (int k = 0; k < LPT; ++k)
+        v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + tid + k * kCopyThreads);
+#pragma unroll
+    for (int k = 0; k < LPT; ++k) reinterpret_cast<u32x4*>(dst)[tid + k * kCopyThreads] = v[k];
+}
+
+template <int LPT>
+__global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
+    const uint8_t* __restrict__ host, const int64_t* __restrict__ blk_off, int32_t B, int32_t k_max,
+    int32_t* __restrict__ table, int32_t max_blocks, const int32_t* __restrict__ free_slots,
+    int32_t* __restrict__ free_head, int32_t n_free, uint8_t* __restrict__ pool, int32_t n_slots, int64_t U,
+    const int32_t* __restrict__ miss_list, const int32_t* __restrict__ miss_cnt,
+    const int32_t* __restrict__ run_cnt, const int32_t* __restrict__ req_err, const int32_t* __restrict__ misc,
+    pulse_recall_stats* __restrict__ stats, int32_t* status) {
+    __shared__ int32_t off[kMaxBatch + 1];
+    __shared__ uint32_t part_sum[kCopyThreads];
+    __shared__ uint32_t sh_runs, sh_bad;
+    const int tid = threadIdx.x;
+    // exclusive scan of miss_cnt: thread t owns a contiguous segment
+    const int per = (B + kCopyThreads - 1) / kCopyThreads;
+    const int s0 = tid * per, s1 = min(B, s0 + per);
+    uint32_t acc = 0, racc = 0, bad = 0;
+    for (int i = s0; i < s1; ++i) {
+        acc += (uint32_t)miss_cnt[i];
+        racc += (uint32_t)run_cnt[i];
+        bad |= (uint32_t)(req_err[i] != 0);
+    }
+    part_sum[tid] = acc;
+    if (tid == 0) { sh_runs = 0; sh_bad = 0; }
+    __syncthreads();
+    if (racc) atomicAdd(&sh_runs, racc);
+    if (bad) atomicOr(&sh_bad, 1u);
+    uint32_t before = 0;
+    for (int t = 0; t < tid; ++t) before += part_sum[t];
+    for (int i = s0; i < s1; ++i) {
+        off[i] = (int32_t)before;
+        before += (uint32_t)miss_cnt[i];
+    }
+    if (tid == kCopyThreads - 1) off[B] = (int32_t)before;
+    __syncthreads();
+    const int64_t total = off[B];
+    const int32_t fh0 = misc[0];
+    const bool ok = sh_bad == 0;
+    const bool fits = fh0 >= 0 && fh0 <= n_free && total <= (int64_t)n_free - fh0;
+    if (blockIdx.x == 0 && tid == 0) {
+        stats->n_missing = (int32_t)total;
+        stats->n_runs = (int32_t)sh_runs;
+        stats->bytes = (ok && fits) ? total * U : 0;
+        if (ok && !fits) report(status, PULSE_ERR_POOL_EXHAUSTED);
+        if (ok && fits) *free_head = fh0 + (int32_t)total;
+    }
+    if (!ok || !fits) return;
+    constexpr int64_t chunk = 4096 * LPT;
+    const int64_t cpb = U / chunk;
+    const int64_t n_chunks = total * cpb;
+    for (int64_t c = blockIdx.x; c < n_chunks; c += gridDim.x) {
+        const int64_t g = c / cpb;
+        const int64_t part = c - g * cpb;
+        int lo = 0, hi = B;  // largest r with off[r] <= g
+        while (hi - lo > 1) {
+            const int mid = (lo + hi) >> 1;
+            if (off[mid] <= g) lo = mid; else hi = mid;
+        }
+        const int r = lo;
+        const int32_t j = miss_list[(size_t)r * k_max + (g - off[r])];
+        const int32_t slot = free_slots[fh0 + g];
+        if (slot < 0 || slot >= n_slots) {
+            if (tid == 0 && part == 0) report(status, PULSE_ERR_BAD_INDEX);
+            continue;
+        }
+        const uint8_t* src = host + (blk_off[r] + j) * U + part * chunk;
+        uint8_t* dst = pool + (int64_t)slot * U + part * chunk;
+        copy_chunk<LPT>(src, dst, tid);
+        if (part == 0 && tid == 0) table[(size_t)r * max_blocks + j] = slot;
+    }
+}
+
+// streaming host -> device copy with the load pattern of the recall kernel
+__global__ __launch_bounds__(kCopyThreads) void probe_copy_kernel(const uint8_t* __restrict__ src,
+                                                                 uint8_t* __restrict__ dst, int64_t n_chunks) {
+    for (int64_t c = blockIdx.x; c < n_chunks; c += gridDim.x)
+        copy_chunk<4>(src + c * 16384, dst + c * 16384, threadIdx.x);
+}
+
+hipError_t launch_recall_plan(const int64_t* blk_off, int32_t B, const int32_t* sel_idx, const int32_t* sel_cnt,
+                              int32_t k_max, const int32_t* table, int32_t max_blocks, int32_t n_slots,
+                              const int32_t* free_head, int32_t* miss_list, int32_t* miss_cnt, int32_t* run_cnt,
+                              int32_t* req_err, int32_t* misc, int32_t* status, hipStream_t st) {
+    if (B == 0) return hipSuccess;
+    hipLaunchKernelGGL(recall_plan_kernel, dim3(B), dim3(kPlanThreads), 0, st, blk_off, sel_idx, sel_cnt, k_max,
+                       table, max_blocks, n_slots, free_head, miss_list, miss_cnt, run_cnt, req_err, misc, status);
+    return hipGetLastError();
+}
+
+hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32_t B, int32_t k_max, int32_t* table,
+                              int32_t max_blocks, const int32_t* free_slots, int32_t* free_head, int32_t n_free,
+                              void* pool, int32_t n_slots, size_t unit_bytes, const int32_t* miss_list,
+                              const int32_t* miss_cnt, const int32_t* run_cnt, const int32_t* req_err,
+                              const int32_t* misc, pulse_recall_stats* stats, int32_t* status, hipStream_t st) {
+    if (B == 0) return hipSuccess;
+    const bool lpt4 = (unit_bytes % 16384) == 0;
+    const int64_t chunk = lpt4 ? 16384 : 8192;
+    const int64_t max_chunks = (int64_t)B * k_max * (int64_t)(unit_bytes / chunk);
+    const unsigned grid = (unsigned)(max_chunks < 2048 ? (max_chunks > 0 ? max_chunks : 1) : 2048);
+    if (lpt4)
+        hipLaunchKernelGGL(recall_copy_kernel<4>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,
+                           blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool,
+                           n_slots, (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status);
+    else
+        hipLaunchKernelGGL(recall_copy_kernel<2>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,
+                           blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool,
+                           n_slots, (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st) {
+    const int64_t n_chunks = (int64_t)(bytes / 16384);
+    if (n_chunks == 0) return hipSuccess;
+    const unsigned grid = (unsigned)(n_chunks < 2048 ? n_chunks : 2048);
+    hipLaunchKernelGGL(probe_copy_kernel, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)src, (uint8_t*)dst,
+                       n_chunks);
+    return hipGetLastError();
+}
+
+}  // namespace pulse

@@ -1,0 +1,193 @@
+"""Device-side state of one layer-step for a generated workload.
+
+Owns the buffers the C ABI operates on (torch device tensors and a pinned,
+host-mapped KV store), the pristine copies needed to restore the block table
+and free-list head between steps, and ready-made argument packs.  Used by the
+tests, the smoke check and the benchmark; it does no compute of its own
+beyond the caller-side setup (uploads and state restores).
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Optional
+
+import numpy as np
+import torch
+
+from . import pulse as P
+from .workloads import Workload
+
+
+class PinnedStore:
+    """Pinned, host-mapped memory from pulse_host_alloc, viewable as numpy."""
+
+    def __init__(self, nbytes: int, coherent: bool = True):
+        self.nbytes = int(nbytes)
+        self.ptr = P.pulse_host_alloc(max(self.nbytes, 1), coherent)
+        self.coherent = coherent
+
+    def numpy(self, shape, dtype) -> np.ndarray:
+        n = int(np.prod(shape)) * np.dtype(dtype).itemsize
+        if n > self.nbytes:
+            raise ValueError("view larger than the pinned allocation")
+        buf = (ctypes.c_char * max(n, 1)).from_address(self.ptr)
+        return np.frombuffer(buf, dtype=dtype, count=int(np.prod(shape))).reshape(shape)
+
+    def free(self):
+        if self.ptr:
+            P.pulse_host_free(self.ptr)
+            self.ptr = 0
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def pinned_allocator(holder: list, coherent: bool = True):
+    """kv_alloc callback for workloads.generate that places the store in pinned memory."""
+
+    def alloc(shape, dtype):
+        store = PinnedStore(int(np.prod(shape)) * np.dtype(dtype).itemsize, coherent)
+        holder.append(store)
+        return store.numpy(shape, dtype)
+
+    return alloc
+
+
+def _dev(a: np.ndarray, device) -> torch.Tensor:
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(device)
+
+
+class LayerState:
+    """All device buffers of one layer-step of workload ``w``.
+
+    host_ptr: address of the pinned host-mapped store holding ``w.kv`` (the
+    workload must have been generated into it)."""
+
+    def __init__(self, w: Workload, host_ptr: int, device="cuda", k_max: Optional[int] = None,
+                 build_digests: bool = True):
+        self.w = w
+        self.device = torch.device(device)
+        self.shape = P.make_shape(w.Hq, w.Hkv, w.d, w.bs, w.dtype_code)
+        self.host_ptr = int(host_ptr)
+        self.k_max = int(k_max or w.k_max)
+        dev = self.device
+        self.ctx_len = _dev(w.ctx_len, dev)
+        self.blk_off = _dev(w.blk_off, dev)
+        self.q = _dev(w.q, dev)
+        self.k_mid = _dev(w.k_mid, dev)
+        self.table0 = _dev(w.table0, dev)
+        self.table = self.table0.clone()
+        self.free_slots = _dev(w.free_slots, dev) if w.free_slots.size else torch.zeros(1, dtype=torch.int32,
+                                                                                        device=dev)
+        self.free_head0 = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.free_head = self.free_head0.clone()
+        E = w.elems_per_block
+        self.pool = torch.zeros((w.n_slots, E), dtype=torch.int16, device=dev)
+        if w.resident_blocks.size:
+            self.pool[: w.resident_blocks.size] = _dev(w.kv[w.resident_blocks], dev)
+        self.sel_idx = torch.full((w.B, self.k_max), -1, dtype=torch.int32, device=dev)
+        self.sel_cnt = torch.zeros(w.B, dtype=torch.int32, device=dev)
+        self.stats = torch.zeros(2, dtype=torch.int64, device=dev)  # pulse_recall_stats (16 bytes)
+        self.dev_status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.out = torch.zeros((w.B, w.Hq, w.d), dtype=torch.float32, device=dev)
+        self.lse = torch.zeros((w.B, w.Hq), dtype=torch.float32, device=dev)
+        self.ws_bytes = P.pulse_workspace_bytes(self.shape, w.B, self.k_max, w.total_blocks)
+        self.ws = torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self.digests = torch.zeros((max(w.total_blocks, 1), 2, w.d), dtype=torch.int16, device=dev)
+        if build_digests:
+            self.build_digests(w.solo_kv_head)
+
+    # ------------------------------------------------------------------ steps
+    def build_digests(self, kv_head: int, out: Optional[torch.Tensor] = None, stream=None):
+        w = self.w
+        dst = self.digests if out is None else out
+        P.pulse_build_digests(self.shape, self.host_ptr, self.blk_off, self.ctx_len, w.B, w.total_blocks, kv_head,
+                              dst, self.dev_status, stream=stream)
+        return dst
+
+    def reset(self):
+        """Restore the block table and free-list head of the step's start; clear status."""
+        self.table.copy_(self.table0)
+        self.free_head.copy_(self.free_head0)
+        self.dev_status.zero_()
+
+    def layer_args(self, digests: Optional[torch.Tensor] = None) -> P.pulse_layer_args:
+        w = self.w
+        a = P.pulse_layer_args()
+        a.shape = self.shape
+        a.B = w.B
+        a.total_blocks = w.total_blocks
+        a.ctx_len = self.ctx_len.data_ptr()
+        a.blk_off = self.blk_off.data_ptr()
+        a.q = self.q.data_ptr()
+        a.digests = (self.digests if digests is None else digests).data_ptr()
+        a.solo_kv_head = w.solo_kv_head
+        a.k_mid = self.k_mid.data_ptr()
+        a.n_sink_blocks = w.n_sink
+        a.n_local_blocks = w.n_local
+        a.k_max = self.k_max
+        a.sel_idx = self.sel_idx.data_ptr()
+        a.sel_cnt = self.sel_cnt.data_ptr()
+        a.host_kv = self.host_ptr
+        a.block_table = self.table.data_ptr()
+        a.max_blocks = w.max_blocks
+        a.free_slots = self.free_slots.data_ptr()
+        a.free_head = self.free_head.data_ptr()
+        a.n_free = int(w.free_slots.size)
+        a.slot_pool = self.pool.data_ptr()
+        a.n_slots = w.n_slots
+        a.stats = self.stats.data_ptr()
+        a.sm_scale = w.sm_scale
+        a.out = self.out.data_ptr()
+        a.lse = self.lse.data_ptr()
+        a.dev_status = self.dev_status.data_ptr()
+        a.ws = self.ws.data_ptr()
+        a.ws_bytes = self.ws_bytes
+        return a
+
+    def decode_layer(self, stream=None):
+        P.pulse_decode_layer(self.layer_args(), stream=stream)
+
+    def select(self, scores: Optional[torch.Tensor] = None, stream=None):
+        w = self.w
+        P.pulse_select_solohead(self.shape, self.q, self.digests, self.blk_off, w.B, w.total_blocks, w.solo_kv_head,
+                                self.k_mid, w.n_sink, w.n_local, self.k_max, self.sel_idx, self.sel_cnt, scores,
+                                self.dev_status, self.ws, self.ws_bytes, stream=stream)
+
+    def recall(self, stream=None):
+        w = self.w
+        P.pulse_recall_gather(self.shape, self.host_ptr, self.blk_off, w.B, self.sel_idx, self.sel_cnt, self.k_max,
+                              self.table, w.max_blocks, self.free_slots, self.free_head, int(w.free_slots.size),
+                              self.pool, w.n_slots, self.stats, self.dev_status, self.ws, self.ws_bytes,
+                              stream=stream)
+
+    def attention(self, stream=None):
+        w = self.w
+        P.pulse_sparse_decode_attn(self.shape, self.q, self.pool, w.n_slots, self.table, w.max_blocks, self.sel_idx,
+                                   self.sel_cnt, self.k_max, self.ctx_len, w.B, w.sm_scale, self.out, self.lse,
+                                   self.dev_status, self.ws, self.ws_bytes, stream=stream)
+
+    # ------------------------------------------------------------------ readback
+    def status(self) -> int:
+        return int(self.dev_status.item())
+
+    def recall_stats(self):
+        s = self.stats.cpu().numpy()
+        n_missing = int(s[0] & 0xFFFFFFFF)
+        n_runs = int((s[0] >> 32) & 0xFFFFFFFF)
+        return n_missing, n_runs, int(s[1])
+
+    def selection(self):
+        return self.sel_idx.cpu().numpy(), self.sel_cnt.cpu().numpy()
+
+    def table_np(self):
+        return self.table.cpu().numpy()
+
+    def pool_np(self) -> np.ndarray:
+        return self.pool.cpu().numpy().view(np.uint16)

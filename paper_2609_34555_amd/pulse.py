@@ -1,0 +1,237 @@
+"""ctypes binding of libpulse.so (include/pulse.h), argument marshalling only.
+
+Every function has the name of its C entry point and forwards plain pointers:
+a torch tensor argument passes ``tensor.data_ptr()``, an int passes itself,
+None passes NULL.  ``stream`` defaults to torch's current HIP stream.  A
+non-OK status raises PulseError.  All compute runs in the library's kernels;
+there is no fallback: a missing library raises at import of the first call.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpulse.so")
+
+PULSE_OK = 0
+PULSE_ERR_INVALID_ARG = 1
+PULSE_ERR_UNSUPPORTED = 2
+PULSE_ERR_WORKSPACE = 3
+PULSE_ERR_POOL_EXHAUSTED = 4
+PULSE_ERR_SELECT_OVERFLOW = 5
+PULSE_ERR_HIP = 6
+PULSE_ERR_BAD_INDEX = 7
+PULSE_F16 = 0
+PULSE_BF16 = 1
+
+EXPORTED = (
+    "pulse_status_string", "pulse_block_bytes", "pulse_workspace_bytes", "pulse_build_digests",
+    "pulse_select_solohead", "pulse_recall_gather", "pulse_sparse_decode_attn", "pulse_decode_layer",
+    "pulse_host_alloc", "pulse_host_free", "pulse_baseline_memcpy_units", "pulse_probe_host_read",
+    "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms",
+)
+
+
+class PulseError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class pulse_shape(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class pulse_recall_stats(ctypes.Structure):
+    _fields_ = [("n_missing", ctypes.c_int32), ("n_runs", ctypes.c_int32), ("bytes", ctypes.c_int64)]
+
+
+_P = ctypes.c_void_p
+
+
+class pulse_layer_args(ctypes.Structure):
+    _fields_ = [
+        ("shape", pulse_shape), ("B", ctypes.c_int32), ("total_blocks", ctypes.c_int64), ("ctx_len", _P),
+        ("blk_off", _P), ("q", _P), ("digests", _P), ("solo_kv_head", ctypes.c_int32), ("k_mid", _P),
+        ("n_sink_blocks", ctypes.c_int32), ("n_local_blocks", ctypes.c_int32), ("k_max", ctypes.c_int32),
+        ("sel_idx", _P), ("sel_cnt", _P), ("host_kv", _P), ("block_table", _P), ("max_blocks", ctypes.c_int32),
+        ("free_slots", _P), ("free_head", _P), ("n_free", ctypes.c_int32), ("slot_pool", _P),
+        ("n_slots", ctypes.c_int32), ("stats", _P), ("sm_scale", ctypes.c_float), ("out", _P), ("lse", _P),
+        ("dev_status", _P), ("ws", _P), ("ws_bytes", ctypes.c_size_t), ("events", _P),
+    ]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libpulse.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        # torch bundles a HIP runtime with the same soname as /opt/rocm's; loading torch
+        # first makes libpulse bind to that one runtime instead of mapping a second copy
+        import torch  # noqa: F401
+
+        L = ctypes.CDLL(LIB_PATH)
+        I32, I64, SZ, F = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+        SP = ctypes.POINTER(pulse_shape)
+        sig = {
+            "pulse_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "pulse_block_bytes": (SZ, [SP]),
+            "pulse_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+            "pulse_build_digests": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, _P, _P]),
+            "pulse_select_solohead": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, I32, I32, I32, _P, _P, _P,
+                                                     _P, _P, SZ, _P]),
+            "pulse_recall_gather": (ctypes.c_int, [SP, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
+                                                   _P, _P, SZ, _P]),
+            "pulse_sparse_decode_attn": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, F, _P, _P,
+                                                        _P, _P, SZ, _P]),
+            "pulse_decode_layer": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
+            "pulse_host_alloc": (ctypes.c_int, [SZ, I32, ctypes.POINTER(ctypes.c_void_p)]),
+            "pulse_host_free": (ctypes.c_int, [_P]),
+            "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
+            "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
+            "pulse_events_create": (ctypes.c_int, [I32, _P]),
+            "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
+            "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    if hasattr(x, "ctypes"):  # numpy array (host buffers)
+        return x.ctypes.data
+    raise TypeError(f"cannot pass {type(x)} as a pointer")
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int, where: str, check: bool):
+    if check and status != PULSE_OK:
+        raise PulseError(status, where)
+    return status
+
+
+def status_string(status: int) -> str:
+    return lib().pulse_status_string(int(status)).decode()
+
+
+def make_shape(num_q_heads, num_kv_heads, head_dim, block_size, dtype) -> pulse_shape:
+    return pulse_shape(num_q_heads, num_kv_heads, head_dim, block_size, dtype)
+
+
+def pulse_block_bytes(shape: pulse_shape) -> int:
+    return lib().pulse_block_bytes(ctypes.byref(shape))
+
+
+def pulse_workspace_bytes(shape: pulse_shape, B: int, k_max: int, total_blocks: int) -> int:
+    return lib().pulse_workspace_bytes(ctypes.byref(shape), B, k_max, total_blocks)
+
+
+def pulse_build_digests(shape, kv, blk_off, ctx_len, B, total_blocks, kv_head, digests, dev_status=None,
+                        stream=None, check=True):
+    st = lib().pulse_build_digests(ctypes.byref(shape), _ptr(kv), _ptr(blk_off), _ptr(ctx_len), B, total_blocks,
+                                   kv_head, _ptr(digests), _ptr(dev_status), _stream(stream))
+    return _check(st, "pulse_build_digests", check)
+
+
+def pulse_select_solohead(shape, q, digests, blk_off, B, total_blocks, solo_kv_head, k_mid, n_sink_blocks,
+                          n_local_blocks, k_max, sel_idx, sel_cnt, scores, dev_status, ws, ws_bytes, stream=None,
+                          check=True):
+    st = lib().pulse_select_solohead(ctypes.byref(shape), _ptr(q), _ptr(digests), _ptr(blk_off), B, total_blocks,
+                                     solo_kv_head, _ptr(k_mid), n_sink_blocks, n_local_blocks, k_max, _ptr(sel_idx),
+                                     _ptr(sel_cnt), _ptr(scores), _ptr(dev_status), _ptr(ws), ws_bytes,
+                                     _stream(stream))
+    return _check(st, "pulse_select_solohead", check)
+
+
+def pulse_recall_gather(shape, host_kv, blk_off, B, sel_idx, sel_cnt, k_max, block_table, max_blocks, free_slots,
+                        free_head, n_free, slot_pool, n_slots, stats, dev_status, ws, ws_bytes, stream=None,
+                        check=True):
+    st = lib().pulse_recall_gather(ctypes.byref(shape), _ptr(host_kv), _ptr(blk_off), B, _ptr(sel_idx),
+                                   _ptr(sel_cnt), k_max, _ptr(block_table), max_blocks, _ptr(free_slots),
+                                   _ptr(free_head), n_free, _ptr(slot_pool), n_slots, _ptr(stats), _ptr(dev_status),
+                                   _ptr(ws), ws_bytes, _stream(stream))
+    return _check(st, "pulse_recall_gather", check)
+
+
+def pulse_sparse_decode_attn(shape, q, slot_pool, n_slots, block_table, max_blocks, sel_idx, sel_cnt, k_max,
+                             ctx_len, B, sm_scale, out, lse, dev_status, ws, ws_bytes, stream=None, check=True):
+    st = lib().pulse_sparse_decode_attn(ctypes.byref(shape), _ptr(q), _ptr(slot_pool), n_slots, _ptr(block_table),
+                                        max_blocks, _ptr(sel_idx), _ptr(sel_cnt), k_max, _ptr(ctx_len), B,
+                                        float(sm_scale), _ptr(out), _ptr(lse), _ptr(dev_status), _ptr(ws), ws_bytes,
+                                        _stream(stream))
+    return _check(st, "pulse_sparse_decode_attn", check)
+
+
+def pulse_decode_layer(args: pulse_layer_args, stream=None, check=True):
+    st = lib().pulse_decode_layer(ctypes.byref(args), _stream(stream))
+    return _check(st, "pulse_decode_layer", check)
+
+
+def pulse_host_alloc(nbytes: int, coherent: bool = True) -> int:
+    p = ctypes.c_void_p()
+    _check(lib().pulse_host_alloc(nbytes, 1 if coherent else 0, ctypes.byref(p)), "pulse_host_alloc", True)
+    return p.value
+
+
+def pulse_host_free(ptr: int):
+    return _check(lib().pulse_host_free(ptr), "pulse_host_free", True)
+
+
+def pulse_baseline_memcpy_units(host_kv, pool, src_units, dst_units, n, unit_bytes, stream=None, check=True):
+    st = lib().pulse_baseline_memcpy_units(_ptr(host_kv), _ptr(pool), _ptr(src_units), _ptr(dst_units), n,
+                                           unit_bytes, _stream(stream))
+    return _check(st, "pulse_baseline_memcpy_units", check)
+
+
+def pulse_probe_host_read(host_src, dev_dst, nbytes, stream=None, check=True):
+    st = lib().pulse_probe_host_read(_ptr(host_src), _ptr(dev_dst), nbytes, _stream(stream))
+    return _check(st, "pulse_probe_host_read", check)
+
+
+class EventSet:
+    """n HIP events owned by the library's helpers (for pulse_layer_args.events)."""
+
+    def __init__(self, n: int):
+        self.n = n
+        self.arr = (ctypes.c_void_p * n)()
+        _check(lib().pulse_events_create(n, ctypes.cast(self.arr, ctypes.c_void_p)), "pulse_events_create", True)
+
+    @property
+    def ptr(self) -> int:
+        return ctypes.addressof(self.arr)
+
+    def elapsed_ms(self, i: int, j: int) -> float:
+        ms = ctypes.c_float()
+        _check(lib().pulse_event_elapsed_ms(self.arr[i], self.arr[j], ctypes.byref(ms)), "pulse_event_elapsed_ms",
+               True)
+        return ms.value
+
+    def destroy(self):
+        if self.arr is not None:
+            lib().pulse_events_destroy(self.n, ctypes.cast(self.arr, ctypes.c_void_p))
+            self.arr = None

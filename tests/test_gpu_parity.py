@@ -1,0 +1,279 @@
+"""GPU parity: every stage of the gfx950 path against the CPU oracle, through the C ABI.
+
+Sizes are ones the oracle finishes in seconds but that span several tiles of
+every kernel and have ragged tails; edge cases cover empty requests, partial
+last blocks, k >= #blocks, k = 0, everything resident, nothing resident, exact
+duplicate blocks (ties), pool exhaustion and malformed selections."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import pulse_oracle as O
+from paper_2609_34555_amd import pulse as P
+from paper_2609_34555_amd import workloads as W
+
+from parity import (assert_attention_close, assert_recall_equal, assert_selection_ok, build, full_check,
+                    oracle_attention, oracle_recall, oracle_selection, say)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _name(request):
+    say(f"\n[gpu] {request.node.name}")
+    yield
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ digests
+
+@pytest.mark.parametrize("dtype,bs,coherent", [("bf16", 16, True), ("f16", 16, False), ("bf16", 32, True),
+                                               ("f16", 64, True)])
+def test_digests_bitexact_every_head(dtype, bs, coherent):
+    spec, s = W.custom("dg", [1000, 17, 1, 513, 64], Hq=16, Hkv=4, bs=bs, dtype=dtype, k_mid=8)
+    w, st = build(spec, s, coherent=coherent)
+    for h in range(w.Hkv):
+        out = torch.zeros_like(st.digests)
+        st.build_digests(h, out=out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().view(np.uint16)[: w.total_blocks]
+        want = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, h)
+        assert np.array_equal(got, want), f"head {h}"
+    assert st.status() == 0
+
+
+def test_digests_signed_zeros():
+    spec, s = W.custom("z", [48], Hq=8, Hkv=2, bs=16, dtype="f16", k_mid=1)
+    w, st = build(spec, s)
+    K = w.kv.reshape(w.total_blocks, 2, w.Hkv, w.bs, w.d)
+    K[0, 0, 0, :, :] = 0
+    K[0, 0, 0, 3, :64] = 0x8000  # -0 in half of the channels of one token
+    K[1, 0, 0, :, :] = 0x8000
+    K[1, 0, 0, 5, 7] = 0
+    st.build_digests(0)
+    torch.cuda.synchronize()
+    got = st.digests.cpu().numpy().view(np.uint16)[: w.total_blocks]
+    want = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, 0)
+    assert np.array_equal(got, want)
+
+
+# ------------------------------------------------------------------ selection
+
+SELECT_CASES = [
+    # name, ctx_lens, Hq, Hkv, bs, dtype, k_mid, n_sink, n_local
+    ("ragged", [5000, 4096, 17, 0, 2100], 32, 8, 16, "bf16", [40, 3, 7, 5, 500], 1, 8),
+    ("g1_f16", [3000, 700], 8, 8, 16, "f16", 25, 1, 2),
+    ("g12", [2048, 999], 48, 4, 32, "bf16", 11, 2, 2),
+    ("g16_bs64", [9000, 64], 16, 1, 64, "bf16", 30, 0, 0),
+    ("k_ge_n", [400, 300], 32, 8, 16, "bf16", 1000, 1, 8),
+    ("k_zero", [400, 300], 32, 8, 16, "bf16", 0, 1, 8),
+    ("forced_cover", [100, 40], 32, 8, 16, "bf16", 4, 3, 5),
+    ("big_n", [131072, 70000], 32, 8, 16, "bf16", [247, 100], 1, 8),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=[c[0] for c in SELECT_CASES])
+def test_select_parity(case):
+    name, ctx, Hq, Hkv, bs, dtype, k_mid, n_sink, n_local = case
+    spec, s = W.custom(name, ctx, Hq=Hq, Hkv=Hkv, bs=bs, dtype=dtype, k_mid=k_mid, n_sink=n_sink,
+                       n_local=n_local, heavy_per_req=6)
+    w, st = build(spec, s)
+    scores = torch.zeros(max(w.total_blocks, 1), dtype=torch.float32, device="cuda")
+    st.select(scores=scores)
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    dig = st.digests.cpu().numpy().view(np.uint16)[: w.total_blocks]
+    rc, oidx, ocnt, osc = oracle_selection(w, dig)
+    gidx, gcnt = st.selection()
+    ties = assert_selection_ok(w, gidx, gcnt, oidx, ocnt, osc)
+    say(f"  boundary near-ties: {ties}")
+    # scores of middle blocks agree with the exact value to fp32 rounding of a short sum
+    g = scores.cpu().numpy().astype(np.float64)
+    for r in range(w.B):
+        b0, n = int(w.blk_off[r]), int(w.n_blocks[r])
+        lo, hi = b0 + w.n_sink, b0 + n - w.n_local
+        if hi > lo:
+            err = np.abs(g[lo:hi] - osc[lo:hi]) / np.maximum(np.abs(osc[lo:hi]), 1.0)
+            assert err.max() < 4e-6
+
+
+def test_select_duplicate_blocks_take_lowest_index():
+    """21 exact copies of each request's best middle block compete for 7 places: only the
+    lowest-index rule decides, and both sides must pick the same blocks."""
+    spec, s = W.custom("dup", [1600, 1600], Hq=32, Hkv=8, bs=16, dtype="bf16", k_mid=7, n_sink=1, n_local=8,
+                       planted=False)
+    w, st = build(spec, s)
+    dig = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, w.solo_kv_head)
+    sc = O.score(w.q, dig, w.blk_off, w.Hq, w.Hkv, w.d, w.dtype_code, w.solo_kv_head)
+    for r in range(w.B):
+        b0, n = int(w.blk_off[r]), int(w.n_blocks[r])
+        best = b0 + 1 + int(np.argmax(sc[b0 + 1: b0 + n - 8]))
+        for j in range(30, 50):
+            if b0 + j != best:
+                w.kv[b0 + j] = w.kv[best]
+    st.build_digests(w.solo_kv_head)
+    st.select()
+    torch.cuda.synchronize()
+    dig = st.digests.cpu().numpy().view(np.uint16)[: w.total_blocks]
+    rc, oidx, ocnt, osc = oracle_selection(w, dig)
+    gidx, gcnt = st.selection()
+    assert np.array_equal(gidx, oidx) and np.array_equal(gcnt, ocnt)
+    for r in range(w.B):
+        mid = [j for j in gidx[r, : gcnt[r]] if 1 <= j < w.n_blocks[r] - 8]
+        assert len(mid) == 7 and max(mid) < 50
+
+
+def test_select_overflow_reports_and_empties_request():
+    spec, s = W.custom("ovf", [800, 800], Hq=32, Hkv=8, bs=16, k_mid=[5, 30], n_sink=1, n_local=8)
+    w, st = build(spec, s, k_max=20)
+    st.select()
+    torch.cuda.synchronize()
+    assert st.status() == P.PULSE_ERR_SELECT_OVERFLOW
+    gidx, gcnt = st.selection()
+    assert gcnt[1] == 0 and np.all(gidx[1] == -1) and gcnt[0] == 14
+
+
+# ------------------------------------------------------------------ recall
+
+RECALL_CASES = [
+    ("ragged_shuffled", [5000, 4096, 17, 0, 2100], 16, "bf16", 40, 0.10, "shuffled", True),
+    ("noncoherent", [3000, 2500, 2000], 16, "bf16", 60, 0.05, "ascending", False),
+    ("bs32_runs", [30000, 9000], 32, "bf16", 200, 0.03, "ascending", True),
+    ("all_resident", [2000, 1000], 16, "f16", 50, 1.0, "ascending", True),
+    ("none_resident", [2000, 1000], 16, "bf16", 50, 0.0, "shuffled", True),
+    ("hkv1_8k_unit", [4000], 16, "bf16", 30, 0.1, "ascending", True),
+]
+
+
+@pytest.mark.parametrize("case", RECALL_CASES, ids=[c[0] for c in RECALL_CASES])
+def test_recall_parity(case):
+    name, ctx, bs, dtype, k_mid, frac, order, coherent = case
+    Hq, Hkv = (8, 1) if name == "hkv1_8k_unit" else (32, 8)
+    spec, s = W.custom(name, ctx, Hq=Hq, Hkv=Hkv, bs=bs, dtype=dtype, k_mid=k_mid, n_sink=1, n_local=2,
+                       resident_frac=frac, heavy_per_req=20, free_order=order)
+    w, st = build(spec, s, coherent=coherent)
+    st.select()
+    st.recall()
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    gidx, gcnt = st.selection()
+    rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt)
+    assert rc == 0
+    assert_recall_equal(st, table, pool, fh, stats)
+    say(f"  missing={stats[0]} runs={stats[1]} bytes={stats[2]}")
+
+
+def test_recall_pool_exhaustion_leaves_state():
+    spec, s = W.custom("exh", [3000, 3000], Hq=32, Hkv=8, bs=16, k_mid=40, n_sink=1, n_local=8,
+                       resident_frac=0.05, n_free_override=10)
+    w, st = build(spec, s)
+    st.select()
+    pool0 = st.pool.clone()
+    st.recall()
+    torch.cuda.synchronize()
+    assert st.status() == P.PULSE_ERR_POOL_EXHAUSTED
+    assert torch.equal(st.table, st.table0) and int(st.free_head.item()) == 0 and torch.equal(st.pool, pool0)
+    n_missing, _, nbytes = st.recall_stats()
+    assert n_missing > 10 and nbytes == 0
+
+
+def test_recall_rejects_unsorted_and_out_of_range():
+    spec, s = W.custom("bad", [3000, 3000], Hq=32, Hkv=8, bs=16, k_mid=40, n_sink=1, n_local=8)
+    w, st = build(spec, s)
+    st.select()
+    torch.cuda.synchronize()
+    idx = st.sel_idx.clone()
+    st.sel_idx[1, 3], st.sel_idx[1, 4] = idx[1, 4], idx[1, 3]
+    st.recall()
+    torch.cuda.synchronize()
+    assert st.status() == P.PULSE_ERR_BAD_INDEX
+    assert torch.equal(st.table, st.table0) and int(st.free_head.item()) == 0
+    st.reset()
+    st.sel_idx.copy_(idx)
+    st.sel_idx[0, 5] = 10 ** 6  # beyond the request's blocks
+    st.sel_idx[0, 6:] = -1
+    st.sel_cnt[0] = 6
+    st.recall()
+    torch.cuda.synchronize()
+    assert st.status() == P.PULSE_ERR_BAD_INDEX and torch.equal(st.table, st.table0)
+
+
+# ------------------------------------------------------------------ attention
+
+ATTN_CASES = [
+    # name, ctx, Hq, Hkv, bs, dtype, k_mid, planted
+    ("cfg1_like_f16", [4096], 32, 8, 16, "f16", 16, True),
+    ("unplanted_ragged", [5000, 4097, 17, 1, 2100], 32, 8, 16, "bf16", [40, 3, 7, 5, 100], False),
+    ("planted_bs32_g8", [20000, 9000], 64, 8, 32, "bf16", 120, True),
+    ("bs64_g2_f16", [7000, 100], 16, 8, 64, "f16", 33, False),
+    ("g16", [3000], 16, 1, 16, "bf16", 64, False),
+    ("g3", [2500, 333], 24, 8, 16, "bf16", 21, False),
+    ("empty_request", [0, 900], 32, 8, 16, "bf16", 10, False),
+]
+
+
+@pytest.mark.parametrize("case", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+def test_attention_parity_stagewise(case):
+    name, ctx, Hq, Hkv, bs, dtype, k_mid, planted = case
+    spec, s = W.custom(name, ctx, Hq=Hq, Hkv=Hkv, bs=bs, dtype=dtype, k_mid=k_mid, n_sink=1, n_local=2,
+                       resident_frac=0.1, heavy_per_req=5, planted=planted)
+    w, st = build(spec, s)
+    res = full_check(w, st, chained=False)
+    say(f"  attn max err {res['attn_err']}")
+
+
+def test_attention_single_token_is_value_row():
+    spec, s = W.custom("one", [1, 17], Hq=8, Hkv=2, bs=16, dtype="bf16", k_mid=1, n_sink=1, n_local=1)
+    w, st = build(spec, s)
+    st.reset()
+    st.decode_layer()
+    torch.cuda.synchronize()
+    V = w.kv.reshape(w.total_blocks, 2, w.Hkv, w.d, w.bs)[:, 1]
+    got = st.out.cpu().numpy()
+    for hq in range(w.Hq):
+        want = W.to_float(V[0, hq // w.G, :, 0], "bf16")
+        assert np.array_equal(got[0, hq], want)
+
+
+# ------------------------------------------------------------------ chained layer-step
+
+@pytest.mark.parametrize("cid,kw", [
+    (1, {}),
+    (2, dict(ctx_scale=1 / 8)),
+    (3, dict(ctx_scale=1 / 16, batch=6)),
+    (4, dict(ctx_scale=1 / 8, layer=5)),
+    (5, dict(ctx_scale=1 / 16)),
+    (2, dict(ctx_scale=1 / 8, planted=False)),
+])
+def test_decode_layer_presets_scaled(cid, kw):
+    spec, s = W.preset(cid, **kw)
+    w, st = build(spec, s)
+    res = full_check(w, st, chained=True)
+    say(f"  cfg{cid} {kw}: stats={res['stats']} ties={res['ties']} attn_err={res['attn_err']}")
+
+
+def test_decode_layer_is_deterministic():
+    spec, s = W.preset(2, ctx_scale=1 / 8)
+    w, st = build(spec, s)
+    outs = []
+    for _ in range(2):
+        st.reset()
+        st.decode_layer()
+        torch.cuda.synchronize()
+        outs.append((st.out.clone(), st.lse.clone(), st.table.clone(), st.sel_idx.clone(), st.stats.clone()))
+    for a, b in zip(outs[0], outs[1]):
+        assert torch.equal(a, b)
+
+
+def test_decode_layer_config2_full_size():
+    """The benchmark's workload (8 x 32K, bf16) at full size, in the same launch
+    configuration the benchmark times."""
+    spec, s = W.preset(2)
+    w, st = build(spec, s)
+    res = full_check(w, st, chained=True)
+    say(f"  cfg2 full: stats={res['stats']} ties={res['ties']} attn_err={res['attn_err']}")
+    heavy_hit = 0
+    gidx, gcnt = st.selection()
+    for r in range(w.B):
+        heavy_hit += len(set(np.asarray(w.heavy[r]).tolist()) & set(gidx[r, : gcnt[r]].tolist()))
+    assert heavy_hit == sum(len(h) for h in w.heavy)  # SoloHead recovers every planted block
