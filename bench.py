@@ -37,6 +37,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probes", action="store_true", help="skip link probes and memcpy baselines")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--profile", action="store_true",
+                    help="profiler run: no CPU baseline or link probes; adds one 256 MiB device copy "
+                         "that calibrates the byte counters")
     return ap.parse_args()
 
 
@@ -208,6 +211,18 @@ def main():
     digest_bytes = int(sum(max(0, n - w.n_sink - w.n_local) for n in w.n_blocks.tolist())) * 2 * w.d * 2
 
     extras = {}
+    if args.profile:
+        # calibration kernel for the FETCH_SIZE / WRITE_SIZE counters: 256 MiB read + 256 MiB written
+        a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        a.fill_(3)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        extras["calibration_copy_bytes"] = 256 << 20
+        del a, b
+        args.no_cpu_baseline = True
+        args.no_probes = True
     if not args.no_probes:
         extras["link"] = link_probes(torch, P, st, holder)
         extras["per_block_memcpy_recall"] = memcpy_recall_baseline(torch, P, st, w)
