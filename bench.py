@@ -120,6 +120,27 @@ def memcpy_recall_baseline(torch, P, st, w):
     return {"blocks": len(src), "ms": ms, "GBps": len(src) * w.unit_bytes / (ms * 1e-3) / 1e9}
 
 
+def counter_traffic(kernel):
+    """HBM-side bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
+    passes (scaled by the copy-kernel calibration); None if its sources changed since."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "counters_cfg2.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        k = json.load(f)["kernels"].get(kernel)
+    if not k:
+        return None
+    h = hashlib.sha256()
+    for src in k["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest()[:16] != k["sources_sha256_16"]:
+        return None
+    return {"fetch": k["fetch_bytes"], "write": k["write_bytes"], "total": k["fetch_bytes"] + k["write_bytes"]}
+
+
 def cpu_baseline(w, seconds):
     """The CPU oracle timed on this host, single thread, on whole layer-steps of the same
     workload (digests are per-block state, built once outside the timing)."""
@@ -255,11 +276,14 @@ def main():
                      "peak": PCIE5_X16_GBPS, "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS,
                      "peak_measured": peak_measured,
                      "frac_of_measured": (recall_GBps / peak_measured) if peak_measured else None,
-                     "bytes_per_launch": rbytes, "traffic": None},
+                     "bytes_per_launch": rbytes,
+                     "traffic": (counter_traffic("recall_copy_kernel") or {}).get("total"),
+                     "traffic_split": counter_traffic("recall_copy_kernel")},
         "roofline_hbm_attention": {"bound": "hbm", "achieved": attn_bytes / (mean["attention"] * 1e-3) / 1e9,
                                    "peak": HBM_GBPS, "unit": "GB/s",
                                    "frac": attn_bytes / (mean["attention"] * 1e-3) / 1e9 / HBM_GBPS,
-                                   "bytes_per_launch": attn_bytes},
+                                   "bytes_per_launch": attn_bytes,
+                                   "traffic": (counter_traffic("attn_splitk_kernel") or {}).get("total")},
         "roofline_hbm_score": {"bound": "hbm", "bytes_per_launch": digest_bytes,
                                "achieved": digest_bytes / (mean["score"] * 1e-3) / 1e9, "peak": HBM_GBPS,
                                "unit": "GB/s"},
