@@ -32,6 +32,8 @@ HBM_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
+                    help="workload preset (2 = the default benchmark line)")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -141,7 +143,7 @@ def counter_traffic(kernel):
     return {"fetch": k["fetch_bytes"], "write": k["write_bytes"], "total": k["fetch_bytes"] + k["write_bytes"]}
 
 
-def cpu_baseline(w, seconds):
+def cpu_baseline(w, seconds, sample_note="whole layer-steps of the same workload"):
     """The CPU oracle timed on this host, single thread, on whole layer-steps of the same
     workload (digests are per-block state, built once outside the timing)."""
     import numpy as np
@@ -167,69 +169,97 @@ def cpu_baseline(w, seconds):
         nbytes = stats[2]
     per_step = elapsed / steps
     return {"value": nbytes / per_step / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} whole layer-steps of the same workload (8 requests), single thread",
+            "sample": f"{steps} x {sample_note} ({w.B} requests), single thread",
             "us_per_layer_step": per_step * 1e6}
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: the sparse-KV decode path here has no multi-GPU mode "
-              "(run with --gpus 1)", file=sys.stderr)
-        sys.exit(2)
-    import numpy as np
-    import torch
+WORKLOADS = {
+    1: "1 request x 4096 tokens, block 16, 32 q / 8 KV heads, head_dim 128, fp16, middle budget 16 blocks "
+       "(+1 sink +8 local), 25% resident, 8 planted heavy blocks",
+    2: "8 requests x 32768 tokens, block 16, 32 q / 8 KV heads, head_dim 128, bf16, 2048-token budget "
+       "(1 sink + 8 local + 119 middle blocks), 10% resident, 32 planted heavy blocks/request",
+    3: "32 requests x U[65536,131072] tokens (ragged), block 16, 32 q / 8 KV heads, head_dim 128, bf16, "
+       "4096-token budget, 5% resident, 32 planted heavy blocks/request",
+    4: "32 layers x (16 requests x 65536 tokens), block 16, 32 q / 8 KV heads, head_dim 128, bf16, "
+       "per-(layer, request) budgets lognormal sigma 1 around 2048 tokens clipped to [256, 8192], 10% resident, "
+       "layers on 4 shared host stores; recall of layer l+1 overlaps attention of layer l on two streams",
+    5: "4 requests x 262144 tokens, block 32, 64 q / 8 KV heads, head_dim 128, bf16, 8192-token budget, "
+       "3% resident, heavy blocks in 4 runs of 16 + 64 singletons per request",
+}
+DTYPES = {1: "f16", 2: "bf16", 3: "bf16", 4: "bf16", 5: "bf16"}
 
-    from paper_2609_34555_amd import harness as H
-    from paper_2609_34555_amd import pulse as P
-    from paper_2609_34555_amd import workloads as W
 
-    torch.cuda.set_device(0)
-    spec, seed = W.preset(2)
+def base_line(cid, K, warmup):
+    return {"metric": METRIC, "unit": "GB/s", "n_gpus": 1, "steps": K, "warmup": warmup,
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": DTYPES[cid],
+            "data": "synthetic (seeded N(0,1) K/V/q, planted heavy blocks; no model weights or datasets)"}
+
+
+def timed_steps(torch, P, st, K, warmup):
+    """W untimed steps, then exactly K timed steps (table restore + pulse_decode_layer),
+    bracketed by device synchronisation; per-stage HIP events of every step are read
+    after the timed region."""
+    evs = [P.EventSet(5) for _ in range(K)]
+    plain = st.layer_args()
+    timed = []
+    for e in evs:
+        a = st.layer_args()
+        a.events = e.ptr
+        timed.append(a)
+    for _ in range(warmup):
+        st.reset()
+        P.pulse_decode_layer(plain)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a in timed:
+        st.reset()
+        P.pulse_decode_layer(a)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stage = {"score": [], "select": [], "recall": [], "attention": [], "layer": []}
+    for e in evs:
+        stage["score"].append(e.elapsed_ms(0, 1))
+        stage["select"].append(e.elapsed_ms(1, 2))
+        stage["recall"].append(e.elapsed_ms(2, 3))
+        stage["attention"].append(e.elapsed_ms(3, 4))
+        stage["layer"].append(e.elapsed_ms(0, 4))
+        e.destroy()
+    return wall, {k: statistics.mean(v) for k, v in stage.items()}
+
+
+def rooflines(w, st, mean, rbytes, peak_measured):
+    recall_GBps = rbytes / (mean["recall"] * 1e-3) / 1e9
+    sel = st.sel_cnt.cpu().numpy()
+    attn_bytes = int(sel.sum()) * w.unit_bytes + w.q.nbytes + w.B * w.Hq * w.d * 4
+    digest_bytes = int(sum(max(0, n - w.n_sink - w.n_local) for n in w.n_blocks.tolist())) * 2 * w.d * 2
+    attn = attn_bytes / (mean["attention"] * 1e-3) / 1e9
+    score = digest_bytes / (mean["score"] * 1e-3) / 1e9
+    roof = {"bound": "host_link", "kernel": "recall_copy_kernel", "achieved": recall_GBps, "peak": PCIE5_X16_GBPS,
+            "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS, "peak_measured": peak_measured,
+            "frac_of_measured": (recall_GBps / peak_measured) if peak_measured else None,
+            "bytes_per_launch": rbytes}
+    attn_roof = {"bound": "hbm", "kernel": "attn_splitk_kernel", "achieved": attn, "peak": HBM_GBPS, "unit": "GB/s",
+                 "frac": attn / HBM_GBPS, "bytes_per_launch": attn_bytes}
+    score_roof = {"bound": "hbm", "kernel": "score_kernel", "achieved": score, "peak": HBM_GBPS, "unit": "GB/s",
+                  "frac": score / HBM_GBPS, "bytes_per_launch": digest_bytes}
+    return roof, attn_roof, score_roof
+
+
+def bench_layer(cid, args, torch, P, H, W):
+    spec, seed = W.preset(cid)
     holder = []
     t0 = time.time()
     w = W.generate(spec, seed, kv_alloc=H.pinned_allocator(holder))
     gen_s = time.time() - t0
     st = H.LayerState(w, holder[0].ptr)
     torch.cuda.synchronize()
-
-    ev = P.EventSet(5)
-    args_nt = st.layer_args()
-    args_ev = st.layer_args()
-    args_ev.events = ev.ptr
-    for _ in range(args.warmup):
-        st.reset()
-        P.pulse_decode_layer(args_nt)
-    torch.cuda.synchronize()
-
     K = args.steps
-    stage_ms = {"score": [], "select": [], "recall": [], "attention": [], "layer": []}
-    torch.cuda.synchronize()
-    t_start = time.perf_counter()
-    for _ in range(K):
-        st.reset()
-        P.pulse_decode_layer(args_ev)
-        # events are read after the step is known complete: the next reset is stream-ordered,
-        # so waiting here only removes host-side overlap of consecutive steps
-        torch.cuda.synchronize()
-        stage_ms["score"].append(ev.elapsed_ms(0, 1))
-        stage_ms["select"].append(ev.elapsed_ms(1, 2))
-        stage_ms["recall"].append(ev.elapsed_ms(2, 3))
-        stage_ms["attention"].append(ev.elapsed_ms(3, 4))
-        stage_ms["layer"].append(ev.elapsed_ms(0, 4))
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_start
+    wall, mean = timed_steps(torch, P, st, K, args.warmup)
     status = st.status()
     if status != 0:
         raise RuntimeError(f"device status {P.status_string(status)}")
     n_missing, n_runs, rbytes = st.recall_stats()
     ms_per_step = wall * 1e3 / K
-    mean = {k: statistics.mean(v) for k, v in stage_ms.items()}
-    recall_GBps = rbytes / (mean["recall"] * 1e-3) / 1e9
-    sel = st.sel_cnt.cpu().numpy()
-    attn_bytes = int(sel.sum()) * w.unit_bytes + w.q.nbytes + w.B * w.Hq * w.d * 4
-    digest_bytes = int(sum(max(0, n - w.n_sink - w.n_local) for n in w.n_blocks.tolist())) * 2 * w.d * 2
 
     extras = {}
     if args.profile:
@@ -249,50 +279,130 @@ def main():
         extras["per_block_memcpy_recall"] = memcpy_recall_baseline(torch, P, st, w)
     peak_measured = max([extras["link"]["memcpy_1GiB_GBps"], extras["link"]["kernel_read_1GiB_GBps"]]
                         if "link" in extras else [0.0]) or None
-
-    line = {
-        "metric": METRIC,
+    roof, attn_roof, score_roof = rooflines(w, st, mean, rbytes, peak_measured)
+    if cid == 2:  # the committed counter passes were taken on this workload
+        roof["traffic"] = (counter_traffic("recall_copy_kernel") or {}).get("total")
+        roof["traffic_split"] = counter_traffic("recall_copy_kernel")
+        attn_roof["traffic"] = (counter_traffic("attn_splitk_kernel") or {}).get("total")
+    else:
+        roof["traffic"] = None
+    line = base_line(cid, K, args.warmup)
+    line.update({
         "value": rbytes / (ms_per_step * 1e-3) / 1e9,
-        "unit": "GB/s",
         "us_per_layer_step": mean["layer"] * 1e3,
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
         "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) K/V/q, planted heavy blocks; no model weights or datasets)",
-        "config": {"workload": "8 requests x 32768 tokens, block 16, 32 q / 8 KV heads, head_dim 128, bf16, "
-                               "2048-token budget (1 sink + 8 local + 119 middle blocks), 10% resident, "
-                               "32 planted heavy blocks/request",
-                   "batch": w.B, "context": int(w.ctx_len[0]), "block_size": w.bs, "k_max": w.k_max,
-                   "parallelism": "single GPU"},
+        "config": {"workload": WORKLOADS[cid], "preset": cid, "batch": w.B, "total_blocks": w.total_blocks,
+                   "block_size": w.bs, "k_max": w.k_max, "parallelism": "single GPU"},
         "recall": {"bytes_per_step": rbytes, "blocks": n_missing, "runs": n_runs,
-                   "kernel_GBps": recall_GBps},
+                   "kernel_GBps": roof["achieved"]},
         "stage_us": {k: v * 1e3 for k, v in mean.items()},
-        "roofline": {"bound": "host_link", "kernel": "recall_copy_kernel", "achieved": recall_GBps,
-                     "peak": PCIE5_X16_GBPS, "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS,
-                     "peak_measured": peak_measured,
-                     "frac_of_measured": (recall_GBps / peak_measured) if peak_measured else None,
-                     "bytes_per_launch": rbytes,
-                     "traffic": (counter_traffic("recall_copy_kernel") or {}).get("total"),
-                     "traffic_split": counter_traffic("recall_copy_kernel")},
-        "roofline_hbm_attention": {"bound": "hbm", "achieved": attn_bytes / (mean["attention"] * 1e-3) / 1e9,
-                                   "peak": HBM_GBPS, "unit": "GB/s",
-                                   "frac": attn_bytes / (mean["attention"] * 1e-3) / 1e9 / HBM_GBPS,
-                                   "bytes_per_launch": attn_bytes,
-                                   "traffic": (counter_traffic("attn_splitk_kernel") or {}).get("total")},
-        "roofline_hbm_score": {"bound": "hbm", "bytes_per_launch": digest_bytes,
-                               "achieved": digest_bytes / (mean["score"] * 1e-3) / 1e9, "peak": HBM_GBPS,
-                               "unit": "GB/s"},
+        "roofline": roof,
+        "roofline_hbm_attention": attn_roof,
+        "roofline_hbm_score": score_roof,
         "extras": extras,
         "setup_s": {"generate": gen_s},
-    }
+    })
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
-    ev.destroy()
+    return line
+
+
+def bench_multilayer(args, torch, P, H, W):
+    """Preset 4: a 32-layer decode step.  Timed: the two-stream schedule (recall of
+    layer l+1 overlapping attention of layer l); also reported: the same step chained on
+    one stream, and headwise vs SoloHead recall transfers."""
+    t0 = time.time()
+    ml = H.MultiLayerStep(n_layers=32, n_stores=4)
+    gen_s = time.time() - t0
+    torch.cuda.synchronize()
+    K = args.steps
+
+    def run(fn):
+        for _ in range(args.warmup):
+            ml.reset()
+            fn()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(K):
+            ml.reset()
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / K
+
+    t_overlap = run(ml.run_overlapped)
+    t_chain = run(ml.run_chained)
+    for st in ml.layers:
+        if st.status() != 0:
+            raise RuntimeError(f"device status {P.status_string(st.status())}")
+    per_layer = [st.recall_stats() for st in ml.layers]
+    rbytes = sum(x[2] for x in per_layer)
+    blocks = sum(x[0] for x in per_layer)
+    runs = sum(x[1] for x in per_layer)
+    # stage timing of every layer inside one chained step
+    evs = [P.EventSet(5) for _ in ml.layers]
+    ml.reset()
+    for st, e in zip(ml.layers, evs):
+        a = st.layer_args()
+        a.events = e.ptr
+        P.pulse_decode_layer(a)
+    torch.cuda.synchronize()
+    recall_ms = sum(e.elapsed_ms(2, 3) for e in evs)
+    attn_ms = sum(e.elapsed_ms(3, 4) for e in evs)
+    for e in evs:
+        e.destroy()
+    # headwise vs SoloHead transfers, per layer against the same tables
+    hw_units = hw_runs = 0
+    for st in ml.layers:
+        st.reset()
+        _, _, miss, hruns = st.headwise()
+        hw_units += int(miss.sum().item())
+        hw_runs += int(hruns.sum().item())
+        st.head_digests = None
+    w0 = ml.layers[0].w
+    U = w0.unit_bytes
+    line = base_line(4, K, args.warmup)
+    recall_GBps = rbytes / (recall_ms * 1e-3) / 1e9
+    line.update({
+        "value": rbytes / t_overlap / 1e9,
+        "us_per_layer_step": t_overlap * 1e6 / len(ml.layers),
+        "ms_per_step": t_overlap * 1e3,
+        "config": {"workload": WORKLOADS[4], "preset": 4, "layers": len(ml.layers), "batch": w0.B,
+                   "block_size": w0.bs, "parallelism": "single GPU, two streams"},
+        "recall": {"bytes_per_step": rbytes, "blocks": blocks, "runs": runs, "kernel_GBps": recall_GBps},
+        "schedules_ms": {"two_stream": t_overlap * 1e3, "one_stream_chained": t_chain * 1e3},
+        "headwise_vs_solohead": {
+            "solohead": {"transfers": blocks, "unit_bytes": U, "runs": runs, "bytes": blocks * U},
+            "headwise": {"transfers": hw_units, "unit_bytes": U // w0.Hkv, "runs": hw_runs,
+                         "bytes": hw_units * U // w0.Hkv}},
+        "roofline": {"bound": "host_link", "kernel": "recall_copy_kernel", "achieved": recall_GBps,
+                     "peak": PCIE5_X16_GBPS, "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS,
+                     "bytes_per_launch": rbytes / len(ml.layers), "traffic": None},
+        "attention_ms_per_step": attn_ms,
+        "setup_s": {"generate_and_upload": gen_s},
+    })
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(w0, args.cpu_seconds, "layer 0 of the 32-layer step")
+    return line
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the sparse-KV decode path here has no multi-GPU mode "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2609_34555_amd import harness as H
+    from paper_2609_34555_amd import pulse as P
+    from paper_2609_34555_amd import workloads as W
+
+    torch.cuda.set_device(0)
+    if args.config == 4:
+        line = bench_multilayer(args, torch, P, H, W)
+    else:
+        line = bench_layer(args.config, args, torch, P, H, W)
     print(json.dumps(line), flush=True)
 
 

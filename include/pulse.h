@@ -149,6 +149,31 @@ PULSE_API pulse_status pulse_select_solohead(const pulse_shape* shape, const voi
                                    size_t ws_bytes, pulse_stream_t stream);
 
 /*
+ * a9. Headwise selection, the baseline SoloHead replaces (Sec. 3.4: every KV
+ * head selecting its own blocks fragments recall into per-head transfers;
+ * Sec. 4.4.1 "headwise" strategy).  Every KV head h scores and selects with
+ * its own digests by the rule of pulse_select_solohead, and its selection is
+ * diffed against the shared block table: each missing (head, block) pair is
+ * one transfer of that head's K and V (U / Hkv bytes).
+ *   head_digests [Hkv][total_blocks][2][d] elements (pulse_build_digests per head)
+ *   sel_idx [Hkv][B][k_max], sel_cnt [Hkv][B]        device int32, written
+ *   miss_cnt [Hkv][B]  missing blocks per (head, request), written
+ *   run_cnt  [Hkv][B]  runs of consecutive missing blocks per (head, request)
+ *   ws       pulse_headwise_workspace_bytes() bytes
+ * Nothing is recalled and the table is not changed.  Errors as for
+ * pulse_select_solohead (block indices beyond max_blocks -> BAD_INDEX).
+ */
+PULSE_API size_t pulse_headwise_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t k_max,
+                                                int64_t total_blocks);
+PULSE_API pulse_status pulse_select_headwise(const pulse_shape* shape, const void* q, const void* head_digests,
+                                             const int64_t* blk_off, int32_t B, int64_t total_blocks,
+                                             const int32_t* k_mid, int32_t n_sink_blocks, int32_t n_local_blocks,
+                                             int32_t k_max, const int32_t* block_table, int32_t max_blocks,
+                                             int32_t n_slots, int32_t* sel_idx, int32_t* sel_cnt, int32_t* miss_cnt,
+                                             int32_t* run_cnt, int32_t* dev_status, void* ws, size_t ws_bytes,
+                                             pulse_stream_t stream);
+
+/*
  * a4 + a5 + a6. Set difference, slot allocation and gather-scatter recall
  * (Sec. 2.2: B_recall = B_topk minus B_gpu, then copy from DRAM; Sec. 4.4.2:
  * scattered blocks move as coalesced transfers and land in the KV cache).

@@ -195,27 +195,37 @@ def mam(q, host_kv, blk_off, ctx_len, r, Hq, Hkv, bs, d, dtype, sm_scale, n_sink
     return best, mam_q, mam_h
 
 
-def headwise_counts(kv, q, blk_off, ctx_len, table, Hq, Hkv, bs, d, dtype, k_mid, n_sink, n_local,
-                    k_max):
-    """Headwise-selection baseline (Sec. 3.4, Sec. 4.4.1 'headwise'): every KV head selects
-    its own blocks with its own digests; each missing (head, block) pair is one transfer of
-    one head's K+V.  Returns (units, runs): runs are maximal stretches of consecutive
-    missing blocks within one (request, head)."""
-    units = 0
-    runs = 0
+def missing_counts(sel_idx, sel_cnt, table):
+    """Set difference of a selection against the block table (Sec. 2.2): per request the
+    number of selected blocks whose entry is -1, and the number of maximal runs of
+    consecutive missing block indices.  Returns (units int64 [B], runs int64 [B])."""
+    B = sel_cnt.shape[0]
+    units = np.zeros(B, np.int64)
+    runs = np.zeros(B, np.int64)
+    for r in range(B):
+        prev = -2
+        for j in sel_idx[r, : sel_cnt[r]]:
+            if table[r, j] < 0:
+                units[r] += 1
+                if j != prev + 1:
+                    runs[r] += 1
+                prev = j
+    return units, runs
+
+
+def headwise_select(kv, q, blk_off, ctx_len, Hq, Hkv, bs, d, dtype, k_mid, n_sink, n_local, k_max):
+    """Headwise selection baseline (Sec. 3.4; Sec. 4.4.1 'headwise'): every KV head selects
+    its own blocks with its own digests.  Returns per-head (sel_idx [Hkv,B,k_max],
+    sel_cnt [Hkv,B], scores [Hkv,total_blocks])."""
     B = ctx_len.shape[0]
+    total = int(blk_off[-1])
+    sel = np.full((Hkv, B, k_max), -1, np.int32)
+    cnt = np.zeros((Hkv, B), np.int32)
+    sc = np.zeros((Hkv, total), np.float64)
     for h in range(Hkv):
         dig = build_digests(kv, blk_off, ctx_len, Hkv, bs, d, dtype, h)
-        s = score(q, dig, blk_off, Hq, Hkv, d, dtype, h)
-        rc, sel_idx, sel_cnt = select(s, blk_off, k_mid, n_sink, n_local, k_max)
+        sc[h] = score(q, dig, blk_off, Hq, Hkv, d, dtype, h)
+        rc, sel[h], cnt[h] = select(sc[h], blk_off, k_mid, n_sink, n_local, k_max)
         if rc:
             raise ValueError(f"select failed: {rc}")
-        for r in range(B):
-            prev = -2
-            for j in sel_idx[r, : sel_cnt[r]]:
-                if table[r, j] < 0:
-                    units += 1
-                    if j != prev + 1:
-                        runs += 1
-                    prev = j
-    return units, runs
+    return sel, cnt, sc

@@ -101,6 +101,7 @@ static pulse_status check_select_args(const pulse_shape* shape, const void* q, c
     PULSE_REQUIRE(B >= 0 && total_blocks >= 0 && k_max >= 1, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(n_sink >= 0 && n_local >= 0, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(solo >= 0 && solo < shape->num_kv_heads, PULSE_ERR_INVALID_ARG);
+    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
     if (B == 0) return PULSE_OK;
     PULSE_REQUIRE(q && blk_off && k_mid && sel_idx && sel_cnt && dev_status, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(digests || total_blocks == 0, PULSE_ERR_INVALID_ARG);
@@ -120,10 +121,48 @@ pulse_status pulse_select_solohead(const pulse_shape* shape, const void* q, cons
     float* sc = scores ? scores : at<float>(ws, w.scores);
     hipStream_t hs = (hipStream_t)stream;
     hipError_t e = launch_score(*shape, q, digests, blk_off, B, total_blocks, solo_kv_head, n_sink_blocks,
-                                n_local_blocks, sc, hs);
+                                n_local_blocks, sc, 1, hs);
     if (e != hipSuccess) return PULSE_ERR_HIP;
-    e = launch_select(blk_off, B, sc, k_mid, n_sink_blocks, n_local_blocks, k_max, sel_idx, sel_cnt, nullptr, 0, 0,
-                      nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, dev_status, hs);
+    e = launch_select(blk_off, B, total_blocks, sc, k_mid, n_sink_blocks, n_local_blocks, k_max, sel_idx, sel_cnt,
+                      nullptr, 0, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, dev_status, 1, hs);
+    return hip_status(e);
+}
+
+size_t pulse_headwise_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t k_max, int64_t total_blocks) {
+    if (!shape_supported(shape) || B < 0 || k_max < 0 || total_blocks < 0) return 0;
+    const size_t H = (size_t)shape->num_kv_heads;
+    size_t o = 0;
+    o = align_up(o + sizeof(float) * H * (size_t)total_blocks);    // scores [Hkv][total_blocks]
+    o = align_up(o + sizeof(int32_t) * H * (size_t)B * k_max);     // miss lists [Hkv][B][k_max]
+    o = align_up(o + sizeof(int32_t) * H * (size_t)B);             // plan errors [Hkv][B]
+    return o;
+}
+
+pulse_status pulse_select_headwise(const pulse_shape* shape, const void* q, const void* head_digests,
+                                   const int64_t* blk_off, int32_t B, int64_t total_blocks, const int32_t* k_mid,
+                                   int32_t n_sink_blocks, int32_t n_local_blocks, int32_t k_max,
+                                   const int32_t* block_table, int32_t max_blocks, int32_t n_slots, int32_t* sel_idx,
+                                   int32_t* sel_cnt, int32_t* miss_cnt, int32_t* run_cnt, int32_t* dev_status,
+                                   void* ws, size_t ws_bytes, pulse_stream_t stream) {
+    pulse_status st = check_select_args(shape, q, head_digests, blk_off, B, total_blocks, 0, k_mid, n_sink_blocks,
+                                        n_local_blocks, k_max, sel_idx, sel_cnt, dev_status);
+    if (st != PULSE_OK || B == 0) return st;
+    PULSE_REQUIRE(block_table && miss_cnt && run_cnt && max_blocks >= 1 && n_slots >= 1, PULSE_ERR_INVALID_ARG);
+    const size_t H = (size_t)shape->num_kv_heads;
+    PULSE_REQUIRE(ws && ws_bytes >= pulse_headwise_workspace_bytes(shape, B, k_max, total_blocks),
+                  PULSE_ERR_WORKSPACE);
+    float* sc = at<float>(ws, 0);
+    size_t o = align_up(sizeof(float) * H * (size_t)total_blocks);
+    int32_t* miss_list = at<int32_t>(ws, o);
+    o = align_up(o + sizeof(int32_t) * H * (size_t)B * k_max);
+    int32_t* req_err = at<int32_t>(ws, o);
+    hipStream_t hs = (hipStream_t)stream;
+    hipError_t e = launch_score(*shape, q, head_digests, blk_off, B, total_blocks, 0, n_sink_blocks, n_local_blocks,
+                                sc, (int32_t)H, hs);
+    if (e != hipSuccess) return PULSE_ERR_HIP;
+    e = launch_select(blk_off, B, total_blocks, sc, k_mid, n_sink_blocks, n_local_blocks, k_max, sel_idx, sel_cnt,
+                      block_table, max_blocks, n_slots, nullptr, miss_list, miss_cnt, run_cnt, req_err, nullptr,
+                      dev_status, (int32_t)H, hs);
     return hip_status(e);
 }
 
@@ -212,12 +251,12 @@ pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream
     hipEvent_t* ev = (hipEvent_t*)a->events;
     if (ev && hipEventRecord(ev[0], hs) != hipSuccess) return PULSE_ERR_HIP;
     hipError_t e = launch_score(a->shape, a->q, a->digests, a->blk_off, a->B, a->total_blocks, a->solo_kv_head,
-                                a->n_sink_blocks, a->n_local_blocks, sc, hs);
+                                a->n_sink_blocks, a->n_local_blocks, sc, 1, hs);
     if (e != hipSuccess) return PULSE_ERR_HIP;
     if (ev && hipEventRecord(ev[1], hs) != hipSuccess) return PULSE_ERR_HIP;
-    e = launch_select(a->blk_off, a->B, sc, a->k_mid, a->n_sink_blocks, a->n_local_blocks, a->k_max, a->sel_idx,
-                      a->sel_cnt, a->block_table, a->max_blocks, a->n_slots, a->free_head, miss_list, miss_cnt,
-                      run_cnt, req_err, misc, a->dev_status, hs);
+    e = launch_select(a->blk_off, a->B, a->total_blocks, sc, a->k_mid, a->n_sink_blocks, a->n_local_blocks,
+                      a->k_max, a->sel_idx, a->sel_cnt, a->block_table, a->max_blocks, a->n_slots, a->free_head,
+                      miss_list, miss_cnt, run_cnt, req_err, misc, a->dev_status, 1, hs);
     if (e != hipSuccess) return PULSE_ERR_HIP;
     if (ev && hipEventRecord(ev[2], hs) != hipSuccess) return PULSE_ERR_HIP;
     e = launch_recall_copy(a->host_kv, a->blk_off, a->B, a->k_max, a->block_table, a->max_blocks, a->free_slots,

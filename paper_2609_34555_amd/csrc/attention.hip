@@ -18,11 +18,21 @@
 // accumulation).  P is split into hi + lo 16-bit parts (two MFMAs), which
 // keeps the P.V product at ~2^-16 relative error instead of the 2^-9 of a
 // single bf16 rounding.  Softmax is online per 32-token step in the log2
-// domain.  Partials (m, l, O) per split go to the workspace; a combine
-// kernel merges them into fp32 out and LSE.
+// domain.
+//
+// Merging the splits: a workgroup holds 4 waves = 4 consecutive splits of one
+// (r, h); they merge through LDS.  With one workgroup per (r, h) it writes the
+// result directly.  Otherwise each workgroup writes one partial (m, l, O) to
+// the workspace and a combine kernel merges those few partials with 256
+// threads per (r, h) and independent loads.  (Merging in the last workgroup
+// to finish would need a device-scope release fence per workgroup, which on
+// gfx950 writes back the XCD's L2 and costs more than the extra launch.)
 #include "pulse_internal.h"
 
 namespace pulse {
+
+constexpr int kAttnWaves = 4;
+constexpr int kAttnThreads = kAttnWaves * kWave;
 
 template <int DT>
 struct Mfma;
@@ -60,38 +70,29 @@ __device__ inline typename Mfma<DT>::vec zero_vec() {
     return __builtin_bit_cast(typename Mfma<DT>::vec, u32x4{0, 0, 0, 0});
 }
 
+// Attention of one wave over entries [e0, e0 + ne) of request r, KV head h.
+// Leaves the running max (log2 domain) and the lane-group-reduced sum for
+// query column `col` in m_run / l_run, and O rows g = 4*grp + v in acc.
 template <int DT, int BS>
-__global__ __launch_bounds__(64) void attn_splitk_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ pool, int32_t n_slots,
-    const int32_t* __restrict__ table, int32_t max_blocks, const int32_t* __restrict__ sel_idx,
-    const int32_t* __restrict__ sel_cnt, int32_t k_max, const int32_t* __restrict__ ctx_len, int32_t Hq,
-    int32_t Hkv, int32_t G, int32_t eps, int32_t n_split, float scale_log2, float* __restrict__ ws_o,
-    float2* __restrict__ ws_ml, int32_t* status) {
+__device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16_t* __restrict__ pool,
+                                    int32_t n_slots, const int32_t* __restrict__ table, int32_t max_blocks,
+                                    const int32_t* __restrict__ sel_row, int ctx, int32_t Hq, int32_t Hkv, int32_t G,
+                                    int r, int h, int e0, int ne, float scale_log2, int32_t* status, int lane,
+                                    float& m_run, float& l_run, f32x4 (&acc)[8]) {
     using M = Mfma<DT>;
     using vec = typename M::vec;
-    const int lane = threadIdx.x;
     const int col = lane & 15;  // MFMA column: query head (QK^T), channel (PV)
     const int grp = lane >> 4;  // lane group: 8-channel / 8-token slice
-    const int s = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
-    const size_t unit = ((size_t)r * Hkv + h) * n_split + s;
-
-    int32_t cnt = sel_cnt[r];
-    if (cnt < 0 || cnt > k_max) {
-        if (lane == 0) report(status, PULSE_ERR_BAD_INDEX);
-        cnt = 0;
-    }
-    const int e0 = s * eps;
-    const int ne = min(e0 + eps, cnt) - e0;  // entries of this split
-    if (ne <= 0) {
-        if (lane < G) ws_ml[unit * G + lane] = make_float2(-INFINITY, 0.f);
-        return;
-    }
-    // entry metadata, one entry per lane (eps <= 64)
-    const int ctx = ctx_len[r];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    m_run = -INFINITY;
+    l_run = 0.f;
+    if (ne <= 0) return;
+    // entry metadata, one entry per lane (ne <= 64)
     const int64_t n_r = ((int64_t)ctx + BS - 1) / BS;
     int my_slot = -1, my_nv = 0;
     if (lane < ne) {
-        const int32_t j = sel_idx[(size_t)r * k_max + e0 + lane];
+        const int32_t j = sel_row[e0 + lane];
         if (j >= 0 && j < n_r && j < max_blocks) {
             const int32_t sl = table[(size_t)r * max_blocks + j];
             if (sl >= 0 && sl < n_slots) {
@@ -112,11 +113,6 @@ __global__ __launch_bounds__(64) void attn_splitk_kernel(
     const size_t E = (size_t)2 * Hkv * BS * kHeadDim;
     const size_t k_head = (size_t)h * BS * kHeadDim;
     const size_t v_head = (size_t)Hkv * BS * kHeadDim + (size_t)h * kHeadDim * BS;
-
-    f32x4 acc[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    float m_run = -INFINITY, l_run = 0.f;
     const int tokens = ne * BS;
 
     for (int t0 = 0; t0 < tokens; t0 += kChunkTokens) {
@@ -201,54 +197,121 @@ __global__ __launch_bounds__(64) void attn_splitk_kernel(
     }
     l_run += __shfl_xor(l_run, 16);
     l_run += __shfl_xor(l_run, 32);
-    if (grp == 0 && col < G) ws_ml[unit * G + col] = make_float2(m_run, l_run);
+}
+
+// grid = (workgroups per (r, h), Hkv, B); 4 waves per workgroup, wave w owns
+// split 4*blockIdx.x + w of eps entries.  Dynamic LDS: O [4][G][128] floats
+// then (m, l) [4][G] float2.
+template <int DT, int BS>
+__global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ pool, int32_t n_slots,
+    const int32_t* __restrict__ table, int32_t max_blocks, const int32_t* __restrict__ sel_idx,
+    const int32_t* __restrict__ sel_cnt, int32_t k_max, const int32_t* __restrict__ ctx_len, int32_t Hq,
+    int32_t Hkv, int32_t G, int32_t eps, int32_t n_wg, float scale_log2, float* __restrict__ ws_o,
+    float2* __restrict__ ws_ml, float* __restrict__ out, float* __restrict__ lse, int32_t* status) {
+    extern __shared__ float smem[];
+    float* s_o = smem;                                                           // [4][G][128]
+    float2* s_ml = reinterpret_cast<float2*>(smem + kAttnWaves * G * kHeadDim);  // [4][G]
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int wg = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+    float* out_rh = out + ((size_t)r * Hq + (size_t)h * G) * kHeadDim;
+    float* lse_rh = lse ? lse + (size_t)r * Hq + (size_t)h * G : nullptr;
+
+    int32_t cnt = sel_cnt[r];
+    if (cnt < 0 || cnt > k_max) {
+        if (tid == 0) report(status, PULSE_ERR_BAD_INDEX);
+        cnt = 0;
+    }
+    const int ns = (cnt + eps - 1) / eps;                // non-empty splits of (r, h)
+    const int nwg = (ns + kAttnWaves - 1) / kAttnWaves;  // workgroups with work
+    if (wg >= nwg) {
+        if (cnt == 0 && wg == 0) {  // empty selection: out = 0, lse = -inf
+            for (int i = tid; i < G * kHeadDim; i += kAttnThreads) out_rh[i] = 0.f;
+            if (lse_rh && tid < G) lse_rh[tid] = -INFINITY;
+        }
+        return;
+    }
+    const int s = wg * kAttnWaves + wave;
+    const int e0 = s * eps;
+    const int ne = min(e0 + eps, cnt) - e0;
+    float m_run, l_run;
+    f32x4 acc[8];
+    attend_split<DT, BS>(q, pool, n_slots, table, max_blocks, sel_idx + (size_t)r * k_max, ctx_len[r], Hq, Hkv, G, r,
+                         h, e0, ne, scale_log2, status, lane, m_run, l_run, acc);
+    // wave partials to LDS
+    if (grp == 0 && col < G) s_ml[wave * G + col] = make_float2(m_run, l_run);
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
         const int g = 4 * grp + v;
         if (g < G) {
-            float* o = ws_o + (unit * G + g) * kHeadDim + col;
+            float* o = s_o + (wave * G + g) * kHeadDim + col;
 #pragma unroll
             for (int t = 0; t < 8; ++t) o[16 * t] = acc[t][v];
         }
     }
+    __syncthreads();
+    // merge the 4 waves: thread handles outputs (g, c) = (idx / 128, idx % 128)
+    const size_t unit = ((size_t)r * Hkv + h) * n_wg + wg;
+    for (int idx = tid; idx < G * kHeadDim; idx += kAttnThreads) {
+        const int g = idx / kHeadDim, c = idx % kHeadDim;
+        float Mx = -INFINITY;
+#pragma unroll
+        for (int w = 0; w < kAttnWaves; ++w) Mx = fmaxf(Mx, s_ml[w * G + g].x);
+        float L = 0.f, a = 0.f;
+        if (Mx != -INFINITY) {
+#pragma unroll
+            for (int w = 0; w < kAttnWaves; ++w) {
+                const float2 ml = s_ml[w * G + g];
+                const float wt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - Mx);
+                L += ml.y * wt;
+                a += s_o[(w * G + g) * kHeadDim + c] * wt;
+            }
+        }
+        if (nwg == 1) {
+            out_rh[idx] = Mx == -INFINITY ? 0.f : a / L;
+            if (lse_rh && c == 0) lse_rh[g] = Mx == -INFINITY ? -INFINITY : (Mx + log2f(L)) * 0.69314718055994531f;
+        } else {
+            ws_o[unit * G * kHeadDim + idx] = a;
+            if (c == 0) ws_ml[unit * G + g] = make_float2(Mx, L);
+        }
+    }
 }
 
-// one wavefront per (request, query head); lane owns channels 2*lane, 2*lane+1
-__global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ ws_o,
-                                                           const float2* __restrict__ ws_ml,
-                                                           const int32_t* __restrict__ sel_cnt, int32_t k_max,
-                                                           int32_t B, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps,
-                                                           int32_t n_split, float* __restrict__ out,
-                                                           float* __restrict__ lse) {
-    const int lane = threadIdx.x & 63;
-    const int64_t item = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (item >= (int64_t)B * Hq) return;
-    const int r = (int)(item / Hq), hq = (int)(item % Hq);
-    const int h = hq / G, g = hq % G;
+// Merge the workgroup partials of one (request, KV head): grid = (Hkv, B),
+// 256 threads, thread owns outputs (g, c) = (idx / 128, idx % 128).  Requests
+// whose selection fits one workgroup were finished by the attention kernel.
+__global__ __launch_bounds__(kAttnThreads) void attn_combine_kernel(
+    const float* __restrict__ ws_o, const float2* __restrict__ ws_ml, const int32_t* __restrict__ sel_cnt,
+    int32_t k_max, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps, int32_t n_wg, float* __restrict__ out,
+    float* __restrict__ lse) {
+    const int tid = threadIdx.x, h = blockIdx.x, r = blockIdx.y;
     int32_t cnt = sel_cnt[r];
-    cnt = cnt < 0 ? 0 : (cnt > k_max ? k_max : cnt);
+    if (cnt < 0 || cnt > k_max) cnt = 0;
     const int ns = (cnt + eps - 1) / eps;
-    const size_t u0 = ((size_t)r * Hkv + h) * n_split;
-    float M = -INFINITY;
-    for (int s = 0; s < ns; ++s) M = fmaxf(M, ws_ml[(u0 + s) * G + g].x);
-    float2* o2 = reinterpret_cast<float2*>(out + item * kHeadDim);
-    if (M == -INFINITY) {
-        o2[lane] = make_float2(0.f, 0.f);
-        if (lse && lane == 0) lse[item] = -INFINITY;
-        return;
+    const int nwg = (ns + kAttnWaves - 1) / kAttnWaves;
+    if (nwg <= 1) return;
+    float* out_rh = out + ((size_t)r * Hq + (size_t)h * G) * kHeadDim;
+    float* lse_rh = lse ? lse + (size_t)r * Hq + (size_t)h * G : nullptr;
+    const size_t u0 = ((size_t)r * Hkv + h) * n_wg;
+    for (int idx = tid; idx < G * kHeadDim; idx += kAttnThreads) {
+        const int g = idx / kHeadDim;
+        float Mx = -INFINITY;
+        for (int w = 0; w < nwg; ++w) Mx = fmaxf(Mx, ws_ml[(u0 + w) * G + g].x);
+        float L = 0.f, a = 0.f;
+        if (Mx != -INFINITY) {
+#pragma unroll 8
+            for (int w = 0; w < nwg; ++w) {
+                const float2 ml = ws_ml[(u0 + w) * G + g];
+                const float wt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - Mx);
+                L += ml.y * wt;
+                a += ws_o[(u0 + w) * G * kHeadDim + idx] * wt;
+            }
+        }
+        out_rh[idx] = Mx == -INFINITY ? 0.f : a / L;
+        if (lse_rh && idx % kHeadDim == 0)
+            lse_rh[g] = Mx == -INFINITY ? -INFINITY : (Mx + log2f(L)) * 0.69314718055994531f;
     }
-    float L = 0.f, a0 = 0.f, a1 = 0.f;
-    for (int s = 0; s < ns; ++s) {
-        const float2 ml = ws_ml[(u0 + s) * G + g];
-        if (ml.x == -INFINITY) continue;
-        const float w = exp2f(ml.x - M);
-        L += ml.y * w;
-        const float2 o = reinterpret_cast<const float2*>(ws_o + ((u0 + s) * G + g) * kHeadDim)[lane];
-        a0 += o.x * w;
-        a1 += o.y * w;
-    }
-    o2[lane] = make_float2(a0 / L, a1 / L);
-    if (lse && lane == 0) lse[item] = (M + log2f(L)) * 0.69314718055994531f;
 }
 
 AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
@@ -272,13 +335,14 @@ AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
 }
 
 template <int DT, int BS>
-static void launch_attn_t(dim3 grid, hipStream_t st, const void* q, const void* pool, int32_t n_slots,
+static void launch_attn_t(dim3 grid, size_t lds, hipStream_t st, const void* q, const void* pool, int32_t n_slots,
                           const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
                           int32_t k_max, const int32_t* ctx_len, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps,
-                          int32_t n_split, float scale_log2, float* ws_o, float2* ws_ml, int32_t* status) {
-    hipLaunchKernelGGL((attn_splitk_kernel<DT, BS>), grid, dim3(64), 0, st, (const uint16_t*)q,
+                          int32_t n_wg, float scale_log2, float* ws_o, float2* ws_ml, float* out, float* lse,
+                          int32_t* status) {
+    hipLaunchKernelGGL((attn_splitk_kernel<DT, BS>), grid, dim3(kAttnThreads), lds, st, (const uint16_t*)q,
                        (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, Hkv,
-                       G, eps, n_split, scale_log2, ws_o, ws_ml, status);
+                       G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse, status);
 }
 
 hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
@@ -288,11 +352,13 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
     if (B == 0) return hipSuccess;
     const int32_t Hkv = s.num_kv_heads, Hq = s.num_q_heads, G = Hq / Hkv;
     const AttnPlan p = attn_plan(B, Hkv, k_max, s.block_size);
-    dim3 grid((unsigned)p.n_split, (unsigned)Hkv, (unsigned)B);
+    const int32_t n_wg = (p.n_split + kAttnWaves - 1) / kAttnWaves;
+    dim3 grid((unsigned)n_wg, (unsigned)Hkv, (unsigned)B);
+    const size_t lds = sizeof(float) * kAttnWaves * G * kHeadDim + sizeof(float2) * kAttnWaves * G;
     const float scale_log2 = sm_scale * 1.4426950408889634f;
-#define PULSE_ATTN(DT, BS)                                                                                         \
-    launch_attn_t<DT, BS>(grid, st, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, Hkv, \
-                          G, p.entries_per_split, p.n_split, scale_log2, ws_o, ws_ml, status)
+#define PULSE_ATTN(DT, BS)                                                                                        \
+    launch_attn_t<DT, BS>(grid, lds, st, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, \
+                          Hkv, G, p.entries_per_split, n_wg, scale_log2, ws_o, ws_ml, out, lse, status)
     if (s.dtype == PULSE_BF16) {
         if (s.block_size == 16) PULSE_ATTN(PULSE_BF16, 16);
         else if (s.block_size == 32) PULSE_ATTN(PULSE_BF16, 32);
@@ -304,10 +370,9 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
     }
 #undef PULSE_ATTN
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    const int64_t items = (int64_t)B * Hq;
-    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, ws_o, ws_ml, sel_cnt,
-                       k_max, B, Hq, Hkv, G, p.entries_per_split, p.n_split, out, lse);
+    if (e != hipSuccess || n_wg <= 1) return e;
+    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)Hkv, (unsigned)B), dim3(kAttnThreads), 0, st, ws_o, ws_ml,
+                       sel_cnt, k_max, Hq, Hkv, G, p.entries_per_split, n_wg, out, lse);
     return hipGetLastError();
 }
 

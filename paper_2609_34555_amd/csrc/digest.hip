@@ -95,18 +95,48 @@ __device__ inline float dot2(uint32_t a, uint32_t b, float acc) {
 
 constexpr int kScoreBlocksPerWg = 64;  // 16 groups x 4 iterations
 
+// Largest r in [0, B) with off[r] <= b, over an LDS copy of blk_off.
+__device__ inline int find_request_lds(const int64_t* off, int32_t B, int64_t b) {
+    int lo = 0, hi = B;
+    while (hi - lo > 1) {
+        int mid = (lo + hi) >> 1;
+        if (off[mid] <= b) lo = mid; else hi = mid;
+    }
+    return lo;
+}
+
 // 256 threads = 16 groups of 16 lanes; group gi handles blocks
 // base + gi + 16*it so that consecutive groups stream consecutive digests.
+// blockIdx.y selects the scoring KV head when several heads score at once
+// (headwise selection); with one head it is `solo`.  blk_off is staged in LDS
+// so the request of a block costs no dependent global loads.
 template <int DT, int G>
 __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__ q,
                                                     const uint16_t* __restrict__ digests,
                                                     const int64_t* __restrict__ blk_off, int32_t B,
                                                     int64_t total_blocks, int32_t Hq, int32_t solo,
                                                     int32_t n_sink, int32_t n_local, float* __restrict__ scores) {
+    extern __shared__ int64_t s_off[];
+    const int head = gridDim.y > 1 ? (int)blockIdx.y : solo;
+    digests += (size_t)blockIdx.y * total_blocks * 2 * kHeadDim;
+    scores += (size_t)blockIdx.y * total_blocks;
+    for (int i = threadIdx.x; i <= B; i += 256) s_off[i] = blk_off[i];
+    __syncthreads();
     const int sub = threadIdx.x & 15;
     const int gi = threadIdx.x >> 4;
     const int c8 = sub * 8;
     const int64_t base = (int64_t)blockIdx.x * kScoreBlocksPerWg + gi;
+    // issue the digest loads of all four iterations before any q load
+    u32x4 dmn[4], dmx[4];
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int64_t b = base + 16 * it;
+        if (b < total_blocks) {
+            const u32x4* dg = reinterpret_cast<const u32x4*>(digests + (size_t)b * 2 * kHeadDim);
+            dmn[it] = dg[sub];
+            dmx[it] = dg[16 + sub];
+        }
+    }
     int cur_r = -1;
     int64_t r_lo = 0, r_hi = 0;
     uint32_t qp[G][4], qm[G][4];
@@ -115,10 +145,10 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
         const int64_t b = base + 16 * it;
         if (b >= total_blocks) break;
         if (b >= r_hi || b < r_lo) {
-            cur_r = find_request(blk_off, B, b);
-            r_lo = blk_off[cur_r];
-            r_hi = blk_off[cur_r + 1];
-            const uint16_t* qr = q + ((size_t)cur_r * Hq + (size_t)solo * G) * kHeadDim + c8;
+            cur_r = find_request_lds(s_off, B, b);
+            r_lo = s_off[cur_r];
+            r_hi = s_off[cur_r + 1];
+            const uint16_t* qr = q + ((size_t)cur_r * Hq + (size_t)head * G) * kHeadDim + c8;
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 u32x4 v = *reinterpret_cast<const u32x4*>(qr + (size_t)g * kHeadDim);
@@ -126,23 +156,20 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
                 for (int p = 0; p < 4; ++p) {
                     qp[g][p] = v[p];
                     // 0xFFFF in each half whose q is non-negative (sign bit clear)
-                    uint32_t s = v[p] & 0x80008000u;
-                    qm[g][p] = ~((s >> 15) * 0xFFFFu) ;
+                    const uint32_t sgn = v[p] & 0x80008000u;
+                    qm[g][p] = ~((sgn >> 15) * 0xFFFFu);
                 }
             }
         }
         const int64_t j = b - r_lo;
         const int64_t n = r_hi - r_lo;
         if (j < n_sink || j >= n - n_local) continue;  // forced blocks are not scored
-        const u32x4* dg = reinterpret_cast<const u32x4*>(digests + (size_t)b * 2 * kHeadDim);
-        u32x4 dmn = dg[sub];
-        u32x4 dmx = dg[16 + sub];
         float acc = 0.f;
 #pragma unroll
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                uint32_t sel = (dmx[p] & qm[g][p]) | (dmn[p] & ~qm[g][p]);
+                const uint32_t sel = (dmx[it][p] & qm[g][p]) | (dmn[it][p] & ~qm[g][p]);
                 acc = dot2<DT>(qp[g][p], sel, acc);
             }
 #pragma unroll
@@ -165,7 +192,8 @@ template <int DT, int G>
 static void launch_score_t(dim3 grid, hipStream_t st, const void* q, const void* digests, const int64_t* blk_off,
                            int32_t B, int64_t total, int32_t Hq, int32_t solo, int32_t n_sink, int32_t n_local,
                            float* scores) {
-    hipLaunchKernelGGL((score_kernel<DT, G>), grid, dim3(256), 0, st, (const uint16_t*)q,
+    const size_t lds = sizeof(int64_t) * ((size_t)B + 1);
+    hipLaunchKernelGGL((score_kernel<DT, G>), grid, dim3(256), lds, st, (const uint16_t*)q,
                        (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores);
 }
 
@@ -187,10 +215,10 @@ static void launch_score_dt(int G, dim3 grid, hipStream_t st, const void* q, con
 
 hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
                         int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
-                        float* scores, hipStream_t st) {
+                        float* scores, int32_t heads, hipStream_t st) {
     if (total_blocks == 0) return hipSuccess;
     const int G = s.num_q_heads / s.num_kv_heads;
-    dim3 grid((unsigned)((total_blocks + kScoreBlocksPerWg - 1) / kScoreBlocksPerWg));
+    dim3 grid((unsigned)((total_blocks + kScoreBlocksPerWg - 1) / kScoreBlocksPerWg), (unsigned)heads);
     if (s.dtype == PULSE_BF16)
         launch_score_dt<PULSE_BF16>(G, grid, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
                                     n_local, scores);

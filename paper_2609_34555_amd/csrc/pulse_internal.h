@@ -68,7 +68,7 @@ struct WsLayout {
     size_t run_cnt;    // int32 [B]
     size_t req_err;    // int32 [B]          per-request plan error (0 = ok)
     size_t misc;       // int32 [16]         [0] = free_head snapshot
-    size_t attn_o;     // float [B][Hkv][max_split][G][d]
+    size_t attn_o;     // float [B][Hkv][max_split][G][d]   (per-workgroup partials)
     size_t attn_ml;    // float2 [B][Hkv][max_split][G]
     size_t total;
 };
@@ -89,18 +89,20 @@ hipError_t launch_build_digests(const pulse_shape& s, const void* kv, const int6
                                 const int32_t* ctx_len, int32_t B, int64_t total_blocks, int32_t kv_head,
                                 void* digests, int32_t* status, hipStream_t st);
 
+// heads == 1: score with KV head `solo`; heads == Hkv: every head h scores with
+// its own digests (digests and scores stacked along h).
 hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
                         int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
-                        float* scores, hipStream_t st);
+                        float* scores, int32_t heads, hipStream_t st);
 
 // select (a3); when table != nullptr the set difference (a4) is folded in and
 // the recall plan (miss list, counts, runs, free_head snapshot) is written.
-hipError_t launch_select(const int64_t* blk_off, int32_t B, const float* scores, const int32_t* k_mid,
-                         int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* sel_idx,
+// heads > 1 stacks scores, selections and plans along the head dimension.
+hipError_t launch_select(const int64_t* blk_off, int32_t B, int64_t total_blocks, const float* scores,
+                         const int32_t* k_mid, int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* sel_idx,
                          int32_t* sel_cnt, const int32_t* table, int32_t max_blocks, int32_t n_slots,
-                         const int32_t* free_head, int32_t* miss_list, int32_t* miss_cnt,
-                         int32_t* run_cnt, int32_t* req_err, int32_t* misc, int32_t* status,
-                         hipStream_t st);
+                         const int32_t* free_head, int32_t* miss_list, int32_t* miss_cnt, int32_t* run_cnt,
+                         int32_t* req_err, int32_t* misc, int32_t* status, int32_t heads, hipStream_t st);
 
 hipError_t launch_recall_plan(const int64_t* blk_off, int32_t B, const int32_t* sel_idx,
                               const int32_t* sel_cnt, int32_t k_max, const int32_t* table,

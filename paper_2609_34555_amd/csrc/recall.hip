@@ -20,8 +20,16 @@
 
 namespace pulse {
 
+#ifndef PULSE_RECALL_GRID
+#define PULSE_RECALL_GRID 128  // measured best on MI355X: more workgroups in flight slow the host link
+#endif
+#ifndef PULSE_RECALL_LPT
+#define PULSE_RECALL_LPT 4
+#endif
+
 constexpr int kPlanThreads = 256;
 constexpr int kCopyThreads = 256;
+constexpr int64_t kRecallGrid = PULSE_RECALL_GRID;  // persistent copy workgroups
 constexpr int kMaxBatch = 4096;  // requests per call supported by the copy kernel
 
 __device__ inline uint64_t lanemask_lt_r() {
@@ -196,18 +204,22 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
                               const int32_t* miss_cnt, const int32_t* run_cnt, const int32_t* req_err,
                               const int32_t* misc, pulse_recall_stats* stats, int32_t* status, hipStream_t st) {
     if (B == 0) return hipSuccess;
-    const bool lpt4 = (unit_bytes % 16384) == 0;
-    const int64_t chunk = lpt4 ? 16384 : 8192;
+    // 16-byte loads in flight per thread: the largest of PULSE_RECALL_LPT, 4, 2 whose
+    // 4 KiB * LPT chunk divides the block
+    int lpt = 2;
+    if (PULSE_RECALL_LPT >= 8 && unit_bytes % 32768 == 0) lpt = 8;
+    else if (unit_bytes % 16384 == 0) lpt = 4;
+    const int64_t chunk = 4096 * (int64_t)lpt;
     const int64_t max_chunks = (int64_t)B * k_max * (int64_t)(unit_bytes / chunk);
-    const unsigned grid = (unsigned)(max_chunks < 2048 ? (max_chunks > 0 ? max_chunks : 1) : 2048);
-    if (lpt4)
-        hipLaunchKernelGGL(recall_copy_kernel<4>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,
-                           blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool,
-                           n_slots, (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status);
-    else
-        hipLaunchKernelGGL(recall_copy_kernel<2>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,
-                           blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool,
-                           n_slots, (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status);
+    const unsigned grid = (unsigned)(max_chunks < kRecallGrid ? (max_chunks > 0 ? max_chunks : 1) : kRecallGrid);
+#define PULSE_COPY(L)                                                                                            \
+    hipLaunchKernelGGL(recall_copy_kernel<L>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,    \
+                       blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool, n_slots, \
+                       (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status)
+    if (lpt == 8) PULSE_COPY(8);
+    else if (lpt == 4) PULSE_COPY(4);
+    else PULSE_COPY(2);
+#undef PULSE_COPY
     return hipGetLastError();
 }
 

@@ -6,7 +6,8 @@
 // middle blocks of highest score are chosen, equal scores in ascending
 // block order; the set is emitted ascending.  One 1024-thread workgroup per
 // request:
-//   1. radix select (4 passes of 8 bits, LDS histogram) of the k'-th largest
+//   1. radix select (8-bit passes over an LDS copy of the keys, starting at the
+//      highest byte in which the keys differ) of the k'-th largest
 //      order-preserving key of the fp32 scores -> threshold T and the number
 //      need_eq of keys equal to T that are taken;
 //   2. one ordered pass over the blocks in tiles of 1024 with wave ballots and
@@ -22,26 +23,41 @@ namespace pulse {
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
+constexpr int kKeyCache = 8192;  // middle-block keys kept in LDS (32 KiB); larger requests read L2
 
 __device__ inline uint64_t lanemask_lt() {
     const int lane = threadIdx.x & 63;
     return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
+// grid = (B, heads): blockIdx.x = request, blockIdx.y = selecting head slot
+// (always 0 for SoloHead; 0..Hkv-1 for headwise selection, whose per-head
+// scores, selections and plans are stacked along the head dimension).
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
-    const int64_t* __restrict__ blk_off, const float* __restrict__ scores, const int32_t* __restrict__ k_mid,
-    int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* __restrict__ sel_idx, int32_t* __restrict__ sel_cnt,
-    const int32_t* __restrict__ table, int32_t max_blocks, int32_t n_slots, const int32_t* __restrict__ free_head,
-    int32_t* __restrict__ miss_list, int32_t* __restrict__ miss_cnt, int32_t* __restrict__ run_cnt,
-    int32_t* __restrict__ req_err, int32_t* __restrict__ misc, int32_t* status) {
+    const int64_t* __restrict__ blk_off, int32_t B, int64_t total_blocks, const float* __restrict__ scores,
+    const int32_t* __restrict__ k_mid, int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* __restrict__ sel_idx,
+    int32_t* __restrict__ sel_cnt, const int32_t* __restrict__ table, int32_t max_blocks, int32_t n_slots,
+    const int32_t* __restrict__ free_head, int32_t* __restrict__ miss_list, int32_t* __restrict__ miss_cnt,
+    int32_t* __restrict__ run_cnt, int32_t* __restrict__ req_err, int32_t* __restrict__ misc, int32_t* status) {
+    __shared__ uint32_t skey[kKeyCache];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sh_prefix, sh_kk;
     __shared__ uint32_t wc[kSelWaves][5];
     __shared__ int32_t sh_err;
 
     const int r = blockIdx.x;
+    const int hy = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     const bool plan = table != nullptr;
+    scores += (size_t)hy * total_blocks;
+    sel_idx += (size_t)hy * B * k_max;
+    sel_cnt += (size_t)hy * B;
+    if (plan) {
+        miss_list += (size_t)hy * B * k_max;
+        miss_cnt += (size_t)hy * B;
+        run_cnt += (size_t)hy * B;
+        req_err += (size_t)hy * B;
+    }
     const int64_t b0 = blk_off[r];
     const int64_t n = blk_off[r + 1] - b0;
     const int64_t lo = n_sink, hi = n - n_local;  // middle blocks [lo, hi)
@@ -51,7 +67,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int64_t cnt = (n - nc) + k;
     int32_t* out = sel_idx + (size_t)r * k_max;
 
-    if (plan && r == 0 && tid == 0) misc[0] = *free_head;
+    if (plan && free_head && r == 0 && hy == 0 && tid == 0) misc[0] = *free_head;
     if (tid == 0) sh_err = 0;
 
     if (cnt > k_max) {
@@ -64,50 +80,81 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         return;
     }
 
+    const bool cached = nc <= kKeyCache;
+    const float* msc = scores + b0 + lo;  // middle scores
     const bool all_mid = (k == nc);
     const bool none_mid = (k == 0);
     uint32_t T = 0, need_eq = 0;
     if (!all_mid && !none_mid) {
-        uint32_t prefix = 0, mask = 0, kk = (uint32_t)k;
-        for (int pass = 0; pass < 4; ++pass) {
-            const int shift = 24 - 8 * pass;
-            if (tid < 256) hist[tid] = 0;
-            __syncthreads();
-            for (int64_t j = lo + tid; j < hi; j += kSelThreads) {
-                uint32_t key = key32(scores[b0 + j]);
-                if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
-            }
-            __syncthreads();
-            if (wid == 0) {
-                // lane owns digits 4*lane .. 4*lane+3; find digit d with
-                // above(d) < kk <= above(d) + hist[d], above(d) = #keys with digit > d.
-                uint32_t c[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) c[i] = hist[4 * lane + i];
-                const uint32_t s = c[0] + c[1] + c[2] + c[3];
-                uint32_t x = s;  // inclusive suffix sum over lanes >= lane
-#pragma unroll
-                for (int off = 1; off < 64; off <<= 1) {
-                    uint32_t y = (uint32_t)__shfl_down((int)x, off);
-                    if (lane + off < 64) x += y;
-                }
-                uint32_t above = x - s;
-#pragma unroll
-                for (int i = 3; i >= 0; --i) {
-                    if (above < kk && kk <= above + c[i]) {
-                        sh_prefix = prefix | ((uint32_t)(4 * lane + i) << shift);
-                        sh_kk = kk - above;
-                    }
-                    above += c[i];
-                }
-            }
-            __syncthreads();
-            prefix = sh_prefix;
-            kk = sh_kk;
-            mask |= 255u << shift;
+        // keys to LDS, with the block-wide min and max key
+        uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+        for (int64_t i = tid; i < nc; i += kSelThreads) {
+            const uint32_t key = key32(msc[i]);
+            if (cached) skey[i] = key;
+            kmin = min(kmin, key);
+            kmax = max(kmax, key);
         }
-        T = prefix;
-        need_eq = kk;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, off));
+            kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off));
+        }
+        if (lane == 0) { wc[wid][0] = kmin; wc[wid][1] = kmax; }
+        __syncthreads();
+        kmin = 0xFFFFFFFFu;
+        kmax = 0u;
+        for (int w = 0; w < kSelWaves; ++w) { kmin = min(kmin, wc[w][0]); kmax = max(kmax, wc[w][1]); }
+        __syncthreads();  // wc is reused below
+        const uint32_t diff = kmin ^ kmax;
+        if (diff == 0) {
+            T = kmax;  // every middle key ties: the first k in index order are taken
+            need_eq = (uint32_t)k;
+        } else {
+            // radix passes start at the byte holding the highest bit in which keys differ
+            const int top = 31 - __clz(diff);
+            const int first_shift = (top / 8) * 8;
+            uint32_t mask = first_shift + 8 >= 32 ? 0u : ~((1u << (first_shift + 8)) - 1u);
+            uint32_t prefix = kmax & mask;
+            uint32_t kk = (uint32_t)k;
+            for (int shift = first_shift; shift >= 0; shift -= 8) {
+                if (tid < 256) hist[tid] = 0;
+                __syncthreads();
+                for (int64_t i = tid; i < nc; i += kSelThreads) {
+                    const uint32_t key = cached ? skey[i] : key32(msc[i]);
+                    if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+                }
+                __syncthreads();
+                if (wid == 0) {
+                    // lane owns digits 4*lane .. 4*lane+3; find digit d with
+                    // above(d) < kk <= above(d) + hist[d], above(d) = #keys with digit > d.
+                    uint32_t c[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) c[i] = hist[4 * lane + i];
+                    const uint32_t sum = c[0] + c[1] + c[2] + c[3];
+                    uint32_t x = sum;  // inclusive suffix sum over lanes >= lane
+#pragma unroll
+                    for (int off = 1; off < 64; off <<= 1) {
+                        const uint32_t y = (uint32_t)__shfl_down((int)x, off);
+                        if (lane + off < 64) x += y;
+                    }
+                    uint32_t above = x - sum;
+#pragma unroll
+                    for (int i = 3; i >= 0; --i) {
+                        if (above < kk && kk <= above + c[i]) {
+                            sh_prefix = prefix | ((uint32_t)(4 * lane + i) << shift);
+                            sh_kk = kk - above;
+                        }
+                        above += c[i];
+                    }
+                }
+                __syncthreads();
+                prefix = sh_prefix;
+                kk = sh_kk;
+                mask |= 255u << shift;
+            }
+            T = prefix;
+            need_eq = kk;
+        }
     }
 
     // ordered pass: selection positions, set difference, runs
@@ -118,7 +165,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         const bool in = j < n;
         const bool forced = in && (j < lo || j >= hi);
         const bool middle = in && !forced;
-        const uint32_t key = middle ? key32(scores[b0 + j]) : 0u;
+        uint32_t key = 0u;
+        if (middle && !all_mid && !none_mid) key = cached ? skey[j - lo] : key32(msc[j - lo]);
         const bool gt = middle && (all_mid || (!none_mid && key > T));
         const bool eq = middle && !all_mid && !none_mid && key == T;
         const uint64_t m_eq = __ballot(eq);
@@ -187,15 +235,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     }
 }
 
-hipError_t launch_select(const int64_t* blk_off, int32_t B, const float* scores, const int32_t* k_mid,
-                         int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* sel_idx, int32_t* sel_cnt,
-                         const int32_t* table, int32_t max_blocks, int32_t n_slots, const int32_t* free_head,
-                         int32_t* miss_list, int32_t* miss_cnt, int32_t* run_cnt, int32_t* req_err, int32_t* misc,
-                         int32_t* status, hipStream_t st) {
+hipError_t launch_select(const int64_t* blk_off, int32_t B, int64_t total_blocks, const float* scores,
+                         const int32_t* k_mid, int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* sel_idx,
+                         int32_t* sel_cnt, const int32_t* table, int32_t max_blocks, int32_t n_slots,
+                         const int32_t* free_head, int32_t* miss_list, int32_t* miss_cnt, int32_t* run_cnt,
+                         int32_t* req_err, int32_t* misc, int32_t* status, int32_t heads, hipStream_t st) {
     if (B == 0) return hipSuccess;
-    hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelThreads), 0, st, blk_off, scores, k_mid, n_sink, n_local,
-                       k_max, sel_idx, sel_cnt, table, max_blocks, n_slots, free_head, miss_list, miss_cnt, run_cnt,
-                       req_err, misc, status);
+    hipLaunchKernelGGL(select_kernel, dim3(B, heads), dim3(kSelThreads), 0, st, blk_off, B, total_blocks, scores,
+                       k_mid, n_sink, n_local, k_max, sel_idx, sel_cnt, table, max_blocks, n_slots, free_head,
+                       miss_list, miss_cnt, run_cnt, req_err, misc, status);
     return hipGetLastError();
 }
 

@@ -173,6 +173,28 @@ class LayerState:
                                    self.sel_cnt, self.k_max, self.ctx_len, w.B, w.sm_scale, self.out, self.lse,
                                    self.dev_status, self.ws, self.ws_bytes, stream=stream)
 
+    def headwise(self, stream=None):
+        """Headwise selection of every KV head with its own digests against this step's
+        table (nothing is recalled).  Returns (sel_idx, sel_cnt, miss_cnt, run_cnt) tensors."""
+        w = self.w
+        H = w.Hkv
+        if getattr(self, "head_digests", None) is None:
+            self.head_digests = torch.zeros((H, max(w.total_blocks, 1), 2, w.d), dtype=torch.int16,
+                                            device=self.device)
+            for h in range(H):
+                self.build_digests(h, out=self.head_digests[h], stream=stream)
+        dev = self.device
+        sel_idx = torch.full((H, w.B, self.k_max), -1, dtype=torch.int32, device=dev)
+        sel_cnt = torch.zeros((H, w.B), dtype=torch.int32, device=dev)
+        miss = torch.zeros((H, w.B), dtype=torch.int32, device=dev)
+        runs = torch.zeros((H, w.B), dtype=torch.int32, device=dev)
+        nb = P.pulse_headwise_workspace_bytes(self.shape, w.B, self.k_max, w.total_blocks)
+        ws = torch.zeros(max(nb, 1), dtype=torch.uint8, device=dev)
+        P.pulse_select_headwise(self.shape, self.q, self.head_digests, self.blk_off, w.B, w.total_blocks, self.k_mid,
+                                w.n_sink, w.n_local, self.k_max, self.table, w.max_blocks, w.n_slots, sel_idx, sel_cnt,
+                                miss, runs, self.dev_status, ws, nb, stream=stream)
+        return sel_idx, sel_cnt, miss, runs
+
     # ------------------------------------------------------------------ readback
     def status(self) -> int:
         return int(self.dev_status.item())
@@ -191,3 +213,60 @@ class LayerState:
 
     def pool_np(self) -> np.ndarray:
         return self.pool.cpu().numpy().view(np.uint16)
+
+
+class MultiLayerStep:
+    """A decode step over many layers (preset 4): one LayerState per layer; layers
+    share ``n_stores`` pinned host stores.  ``run_chained`` issues one
+    pulse_decode_layer per layer on one stream.  ``run_overlapped`` keeps only the
+    recalls on an I/O stream: selection of layer l+1 and attention of layer l run on a
+    compute stream while layer l+1's blocks cross the host link (the queries of every
+    layer are given up front)."""
+
+    def __init__(self, n_layers: int = 32, n_stores: int = 4, device="cuda", **preset_kw):
+        from . import workloads as W
+
+        self.layers = []
+        self.stores = {}
+        for layer in range(n_layers):
+            spec, seed = W.preset(4, layer=layer, n_stores=n_stores, **preset_kw)
+            sid = layer % n_stores
+            if sid not in self.stores:
+                holder = []
+                w = W.generate(spec, seed, kv_alloc=pinned_allocator(holder))
+                self.stores[sid] = (w, holder)
+            else:
+                w = W.generate(spec, seed, reuse_kv=self.stores[sid][0])
+            self.layers.append(LayerState(w, self.stores[sid][1][0].ptr, device=device))
+        self.io_stream = torch.cuda.Stream()
+        self.cmp_stream = torch.cuda.Stream()
+        self.selected = [torch.cuda.Event() for _ in self.layers]
+        self.recalled = [torch.cuda.Event() for _ in self.layers]
+
+    def reset(self):
+        for st in self.layers:
+            st.reset()
+
+    def run_chained(self, stream=None):
+        for st in self.layers:
+            st.decode_layer(stream=stream)
+
+    def run_overlapped(self):
+        cur = torch.cuda.current_stream()
+        io, cmp_ = self.io_stream, self.cmp_stream
+        io.wait_stream(cur)
+        cmp_.wait_stream(cur)
+        n = len(self.layers)
+        self.layers[0].select(stream=cmp_)
+        self.selected[0].record(cmp_)
+        for i, st in enumerate(self.layers):
+            io.wait_event(self.selected[i])
+            st.recall(stream=io)
+            self.recalled[i].record(io)
+            if i + 1 < n:  # next layer's selection while this layer's blocks cross the link
+                self.layers[i + 1].select(stream=cmp_)
+                self.selected[i + 1].record(cmp_)
+            cmp_.wait_event(self.recalled[i])
+            st.attention(stream=cmp_)
+        cur.wait_stream(io)
+        cur.wait_stream(cmp_)

@@ -29,7 +29,8 @@ EXPORTED = (
     "pulse_status_string", "pulse_block_bytes", "pulse_workspace_bytes", "pulse_build_digests",
     "pulse_select_solohead", "pulse_recall_gather", "pulse_sparse_decode_attn", "pulse_decode_layer",
     "pulse_host_alloc", "pulse_host_free", "pulse_baseline_memcpy_units", "pulse_probe_host_read",
-    "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms",
+    "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms", "pulse_headwise_workspace_bytes",
+    "pulse_select_headwise",
 )
 
 
@@ -95,6 +96,9 @@ def lib():
             "pulse_host_free": (ctypes.c_int, [_P]),
             "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
             "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
+            "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+            "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
+                                                     _P, _P, _P, _P, _P, SZ, _P]),
             "pulse_events_create": (ctypes.c_int, [I32, _P]),
             "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
             "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
@@ -166,6 +170,21 @@ def pulse_select_solohead(shape, q, digests, blk_off, B, total_blocks, solo_kv_h
                                      _ptr(sel_cnt), _ptr(scores), _ptr(dev_status), _ptr(ws), ws_bytes,
                                      _stream(stream))
     return _check(st, "pulse_select_solohead", check)
+
+
+def pulse_headwise_workspace_bytes(shape: pulse_shape, B: int, k_max: int, total_blocks: int) -> int:
+    return lib().pulse_headwise_workspace_bytes(ctypes.byref(shape), B, k_max, total_blocks)
+
+
+def pulse_select_headwise(shape, q, head_digests, blk_off, B, total_blocks, k_mid, n_sink_blocks, n_local_blocks,
+                          k_max, block_table, max_blocks, n_slots, sel_idx, sel_cnt, miss_cnt, run_cnt, dev_status, ws,
+                          ws_bytes, stream=None, check=True):
+    st = lib().pulse_select_headwise(ctypes.byref(shape), _ptr(q), _ptr(head_digests), _ptr(blk_off), B,
+                                     total_blocks, _ptr(k_mid), n_sink_blocks, n_local_blocks, k_max,
+                                     _ptr(block_table), max_blocks, n_slots, _ptr(sel_idx), _ptr(sel_cnt),
+                                     _ptr(miss_cnt), _ptr(run_cnt), _ptr(dev_status), _ptr(ws), ws_bytes,
+                                     _stream(stream))
+    return _check(st, "pulse_select_headwise", check)
 
 
 def pulse_recall_gather(shape, host_kv, blk_off, B, sel_idx, sel_cnt, k_max, block_table, max_blocks, free_slots,

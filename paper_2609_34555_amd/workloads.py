@@ -10,7 +10,7 @@ Shapes follow the paper's decode workloads: block size 16, head_dim 128,
 bf16 KV, a 2,048-token hot budget of 16 sink + 128 local + 1,904 middle
 tokens (Sec. 5 setup), long contexts of 32K-256K tokens with lognormal-like
 raggedness (Sec. 5 workloads).  Five named presets are provided; see
-``PRESETS``.
+``preset``.
 
 Host KV store layout (one block = all KV heads, K then V):
     K part  [Hkv][bs][d]   token-major
@@ -92,6 +92,7 @@ class Spec:
     free_order: str = "ascending"  # or "shuffled"
     slack_slots: int = 0  # extra free slots beyond the worst case
     n_free_override: Optional[int] = None  # force a small free list (pool exhaustion)
+    resident_key: int = 0  # stream of the resident sample (layers sharing a store differ here)
 
 
 @dataclass
@@ -157,7 +158,7 @@ def _middle_budget(budget_tokens: int, bs: int) -> int:
 
 
 def preset(config_id: int, *, ctx_scale: float = 1.0, batch: Optional[int] = None, layer: int = 0,
-           planted: bool = True, free_order: str = "ascending") -> tuple:
+           planted: bool = True, free_order: str = "ascending", n_stores: int = 4) -> tuple:
     """(Spec, seed) of one of the five named workloads.
 
     1: 1 request x 4096 tokens, bs 16, 32/8 heads, fp16, middle budget 16 blocks,
@@ -166,7 +167,8 @@ def preset(config_id: int, *, ctx_scale: float = 1.0, batch: Optional[int] = Non
     3: 32 requests, contexts uniform in [64K, 128K] (ragged), 4096-token budget,
        5% resident, 32 heavy/request.
     4: one layer of a 32-layer step: 16 x 64K, per-request budgets lognormal
-       (sigma 1) around 2048 tokens clipped to [256, 8192], 10% resident.
+       (sigma 1) around 2048 tokens clipped to [256, 8192], 10% resident; layer l
+       shares host store l % n_stores (keys, values, query) with other layers.
     5: 4 x 256K, bs 32, 64/8 heads, 8192-token budget, 3% resident, heavy blocks
        in 4 runs of 16 plus 64 singletons.
     ctx_scale shrinks contexts (and batch may be overridden) for oracle-sized runs.
@@ -193,12 +195,17 @@ def preset(config_id: int, *, ctx_scale: float = 1.0, batch: Optional[int] = Non
         spec.k_mid = [_middle_budget(4096, 16)] * B
         nh = [32] * B
     elif config_id == 4:
+        # layer l reads host store l % n_stores (keys, values, query, planted blocks);
+        # its budgets and resident set are its own
+        store = layer % n_stores
+        rng = np.random.default_rng([seed, store, 0])
         B = batch or 16
         ctx = [max(1, int(65536 * ctx_scale))] * B
         spec = Spec(f"cfg4_l{layer}", B, ctx, 32, 8, 128, 16, "bf16", resident_frac=0.10)
-        z = rng.standard_normal(B)
+        z = np.random.default_rng([seed, 1000 + layer]).standard_normal(B)
         budgets = np.clip(2048.0 * np.exp(z), 256, 8192)
         spec.k_mid = [int(b) // 16 - 9 for b in budgets]
+        spec.resident_key = layer
         nh = [32] * B
     elif config_id == 5:
         B = batch or 4
@@ -225,7 +232,7 @@ def preset(config_id: int, *, ctx_scale: float = 1.0, batch: Optional[int] = Non
             h = min(nh[r], m)
             heavy.append(np.sort(rng.choice(m, size=h, replace=False)).astype(np.int64) + lo_m)
     spec.heavy = heavy
-    return spec, seed + 7919 * layer
+    return spec, seed + 7919 * (layer % n_stores if config_id == 4 else layer)
 
 
 def _clustered_heavy(rng, lo: int, hi: int, runs: int, run_len: int, singles: int) -> np.ndarray:
@@ -282,10 +289,11 @@ def _fill_chunk(out: np.ndarray, seed_key, dtype: str):
 
 
 def generate(spec: Spec, seed: int, *, kv_alloc: Optional[Callable] = None, threads: Optional[int] = None,
-             store_key: int = 0) -> Workload:
+             store_key: int = 0, reuse_kv: Optional["Workload"] = None) -> Workload:
     """Draw a full workload.  ``kv_alloc(shape, np.uint16)`` may return a view of pinned host
-    memory so the store is generated in place.  ``store_key`` selects the key/value stream
-    (layers that share a host store share it)."""
+    memory so the store is generated in place.  ``store_key`` selects the key/value stream.
+    ``reuse_kv``: a workload drawn with the same seed, contexts and heavy blocks whose store,
+    query and retrieval head are taken as they are (layers sharing one host store)."""
     B = spec.batch
     Hq, Hkv, d, bs, dtype = spec.num_q_heads, spec.num_kv_heads, spec.head_dim, spec.block_size, spec.dtype
     if Hq % Hkv:
@@ -301,6 +309,11 @@ def generate(spec: Spec, seed: int, *, kv_alloc: Optional[Callable] = None, thre
 
     q = round_to_dtype(rng.standard_normal((B, Hq, d), dtype=np.float32), dtype).reshape(B, Hq, d)
     solo = int(rng.integers(Hkv))
+    if reuse_kv is not None:
+        if reuse_kv.seed != seed or not np.array_equal(reuse_kv.blk_off, blk_off):
+            raise ValueError("reuse_kv must come from the same seed and contexts")
+        return _finish(spec, seed, B, Hq, Hkv, d, bs, dtype, ctx_len, n_blocks, blk_off, reuse_kv.q, reuse_kv.kv,
+                       reuse_kv.solo_kv_head)
 
     kv = kv_alloc((total, E), np.uint16) if kv_alloc else np.empty((total, E), np.uint16)
     # bulk N(0,1) keys/values, chunked by request and block range with independent streams
@@ -348,12 +361,17 @@ def generate(spec: Spec, seed: int, *, kv_alloc: Optional[Callable] = None, thre
             kpart[:, nv:, :] = 0
             vpart[:, :, nv:] = 0
 
+    return _finish(spec, seed, B, Hq, Hkv, d, bs, dtype, ctx_len, n_blocks, blk_off, q, kv, solo)
+
+
+def _finish(spec, seed, B, Hq, Hkv, d, bs, dtype, ctx_len, n_blocks, blk_off, q, kv, solo) -> Workload:
+    """Resident hot set, slot pool, free list and budgets of a drawn store."""
     # resident hot set: forced sink/local blocks plus a seeded sample of middle blocks
     k_mid = np.asarray(spec.k_mid, np.int32)
     max_blocks = int(max(1, n_blocks.max() if B else 1))
     table0 = np.full((B, max_blocks), -1, np.int32)
     resident = []
-    rrng = np.random.default_rng([seed, 2])
+    rrng = np.random.default_rng([seed, 2, spec.resident_key])
     for r in range(B):
         n = int(n_blocks[r])
         forced = sorted(set(range(min(spec.n_sink, n))) | set(range(max(0, n - spec.n_local), n)))

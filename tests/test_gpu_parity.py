@@ -277,3 +277,61 @@ def test_decode_layer_config2_full_size():
     for r in range(w.B):
         heavy_hit += len(set(np.asarray(w.heavy[r]).tolist()) & set(gidx[r, : gcnt[r]].tolist()))
     assert heavy_hit == sum(len(h) for h in w.heavy)  # SoloHead recovers every planted block
+
+
+# ------------------------------------------------------------------ headwise selection (a9)
+
+@pytest.mark.parametrize("cid,kw", [(4, dict(ctx_scale=1 / 16, batch=4, layer=3)),
+                                    (2, dict(ctx_scale=1 / 8, batch=3))])
+def test_headwise_selection_and_counts(cid, kw):
+    spec, s = W.preset(cid, **kw)
+    w, st = build(spec, s)
+    sel, cnt, miss, runs = st.headwise()
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    gsel, gcnt = sel.cpu().numpy(), cnt.cpu().numpy()
+    gmiss, gruns = miss.cpu().numpy(), runs.cpu().numpy()
+    osel, ocnt, osc = O.headwise_select(w.kv, w.q, w.blk_off, w.ctx_len, w.Hq, w.Hkv, w.bs, w.d, w.dtype_code,
+                                        w.k_mid, w.n_sink, w.n_local, st.k_max)
+    total_units = 0
+    for h in range(w.Hkv):
+        assert_selection_ok(w, gsel[h], gcnt[h], osel[h], ocnt[h], osc[h])
+        units, nruns = O.missing_counts(gsel[h], gcnt[h], w.table0)
+        assert np.array_equal(gmiss[h], units) and np.array_equal(gruns[h], nruns)
+        total_units += int(units.sum())
+    # SoloHead on the same step: whole blocks, one transfer stream per run
+    st.reset()
+    st.select()
+    st.recall()
+    torch.cuda.synchronize()
+    n_missing, n_runs, nbytes = st.recall_stats()
+    say(f"  solohead: {n_missing} blocks / {n_runs} runs / {nbytes} B;  headwise: {total_units} head-blocks / "
+        f"{int(gruns.sum())} runs / {total_units * w.unit_bytes // w.Hkv} B")
+    assert total_units > n_missing  # heads disagree on most non-planted blocks
+
+
+# ------------------------------------------------------------------ multi-layer step, two streams
+
+def test_multilayer_overlapped_matches_chained_and_oracle():
+    from paper_2609_34555_amd.harness import MultiLayerStep
+
+    ml = MultiLayerStep(n_layers=6, n_stores=2, ctx_scale=1 / 32, batch=4)
+    ml.reset()
+    ml.run_chained()
+    torch.cuda.synchronize()
+    snap = [(st.out.clone(), st.lse.clone(), st.table.clone(), st.stats.clone(), st.sel_idx.clone())
+            for st in ml.layers]
+    ml.reset()
+    ml.run_overlapped()
+    torch.cuda.synchronize()
+    for st, ref in zip(ml.layers, snap):
+        assert st.status() == 0
+        for a, b in zip((st.out, st.lse, st.table, st.stats, st.sel_idx), ref):
+            assert torch.equal(a, b)
+    # layers sharing a store share keys and queries but not budgets or resident sets
+    assert ml.layers[0].w.kv is ml.layers[2].w.kv
+    assert not np.array_equal(ml.layers[0].w.table0, ml.layers[2].w.table0)
+    for i in (0, 3):
+        st = ml.layers[i]
+        res = full_check(st.w, st, chained=True)
+        say(f"  layer {i}: stats={res['stats']} attn_err={res['attn_err']}")
