@@ -92,17 +92,19 @@ def assert_attention_close(st, out, lse, tol=ATTN_TOL):
     return err, lerr
 
 
-def full_check(w, st, chained=True):
-    """Run one layer-step on the GPU (chained or stage by stage) and check every stage."""
-    st.reset()
-    if chained:
-        st.decode_layer()
-    else:
-        st.select()
-        st.recall()
-        st.attention()
+def full_check(w, st, chained=True, run=True):
+    """Run one layer-step on the GPU (chained or stage by stage; run=False checks the
+    state a previous run left) and check every stage against the oracle."""
     import torch
 
+    if run:
+        st.reset()
+        if chained:
+            st.decode_layer()
+        else:
+            st.select()
+            st.recall()
+            st.attention()
     torch.cuda.synchronize()
     assert st.status() == 0, f"device status {st.status()}"
     dig = st.digests.cpu().numpy().view(np.uint16)[: w.total_blocks]
