@@ -143,6 +143,31 @@ def counter_traffic(kernel):
     return {"fetch": k["fetch_bytes"], "write": k["write_bytes"], "total": k["fetch_bytes"] + k["write_bytes"]}
 
 
+def engine_recall_baseline(torch, P, st, w, reps=5):
+    """The paper's recall engine on the same selection: GPU plan + publish into a pinned
+    mailbox, CPU poller and 8 gather threads into pinned staging, one DMA per 16 MiB batch,
+    GPU scatter.  Wall time from submit to the host seeing completion."""
+    eng = P.GatherScatterEngine(st.shape, n_workers=8, max_blocks_per_call=w.B * st.k_max,
+                                staging_blocks=max(1, (16 << 20) // w.unit_bytes))
+    times, timing = [], None
+    try:
+        for _ in range(reps + 1):
+            st.reset()
+            st.select()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            st.recall_gs(eng)
+            times.append((time.perf_counter() - t0) * 1e3)
+            timing = eng.last_timing()
+    finally:
+        eng.destroy()
+    torch.cuda.synchronize()
+    ms = statistics.median(times[1:])
+    nbytes = st.recall_stats()[2]
+    return {"ms": ms, "GBps": nbytes / (ms * 1e-3) / 1e9, "last_call": timing, "workers": 8,
+            "staging_MiB": 16}
+
+
 def cpu_baseline(w, seconds, sample_note="whole layer-steps of the same workload"):
     """The CPU oracle timed on this host, single thread, on whole layer-steps of the same
     workload (digests are per-block state, built once outside the timing)."""
@@ -277,6 +302,7 @@ def bench_layer(cid, args, torch, P, H, W):
     if not args.no_probes:
         extras["link"] = link_probes(torch, P, st, holder)
         extras["per_block_memcpy_recall"] = memcpy_recall_baseline(torch, P, st, w)
+        extras["paper_engine_recall"] = engine_recall_baseline(torch, P, st, w)
     peak_measured = max([extras["link"]["memcpy_1GiB_GBps"], extras["link"]["kernel_read_1GiB_GBps"]]
                         if "link" in extras else [0.0]) or None
     roof, attn_roof, score_roof = rooflines(w, st, mean, rbytes, peak_measured)

@@ -63,8 +63,9 @@ typedef enum {
     PULSE_ERR_POOL_EXHAUSTED = 4,  /* device-detected: more missing blocks than free slots */
     PULSE_ERR_SELECT_OVERFLOW = 5, /* device-detected: forced + k_mid blocks exceed k_max */
     PULSE_ERR_HIP = 6,             /* a HIP launch or runtime call failed */
-    PULSE_ERR_BAD_INDEX = 7        /* device-detected: block/slot index outside its buffer,
+    PULSE_ERR_BAD_INDEX = 7,       /* device-detected: block/slot index outside its buffer,
                                       or a selection list not strictly ascending */
+    PULSE_ERR_TIMEOUT = 8          /* host-side wait expired (gather-scatter engine) */
 } pulse_status;
 
 typedef enum { PULSE_F16 = 0, PULSE_BF16 = 1 } pulse_dtype;
@@ -204,6 +205,50 @@ PULSE_API pulse_status pulse_recall_gather(const pulse_shape* shape, const void*
                                  int32_t* free_head, int32_t n_free, void* slot_pool, int32_t n_slots,
                                  pulse_recall_stats* stats, int32_t* dev_status, void* ws,
                                  size_t ws_bytes, pulse_stream_t stream);
+
+/*
+ * The paper's own recall engine as a second recall path (Sec. 4.4.2:
+ * gather the scattered blocks on the CPU into a contiguous pinned staging
+ * buffer, move them with one large DMA, scatter them into the GPU KV cache
+ * with a GPU kernel; Sec. 4.5: zero-sync submission -- the GPU writes the
+ * selected indices and a ready flag into host-visible memory and a CPU
+ * polling thread builds the recall task for I/O worker threads).
+ *
+ * pulse_gs_engine_create: one engine per device and shape.  Owns a pinned
+ *   mailbox for up to max_blocks_per_call plan entries, two pinned and two
+ *   device staging buffers of staging_blocks blocks each (double-buffered
+ *   batches), an I/O stream, n_workers gather threads and a poller thread.
+ *   Allocation happens here, never in the calls below.
+ * pulse_gs_recall_submit: same arguments and results as
+ *   pulse_recall_gather (set difference, allocation, table / free_head /
+ *   stats updates on `stream`), but the bytes move through the engine.
+ *   Returns at once with a sequence number; one call may be in flight per
+ *   engine (a second submit before completion -> PULSE_ERR_INVALID_ARG).
+ *   The pool slots are valid once the call has completed.
+ * pulse_gs_recall_poll: non-blocking completion check (*done = 1 when the
+ *   blocks are in the pool; returns that call's device-detected status).
+ * pulse_gs_recall_wait: blocks up to timeout_ms; PULSE_ERR_TIMEOUT if the
+ *   call has not completed.  No GPU stream waits on the host: the caller
+ *   enqueues attention after completion (the semi-synchronous check of
+ *   Sec. 4.2.2 is a poll at a layer boundary).
+ * pulse_gs_last_timing: milliseconds of the last completed call: CPU gather,
+ *   the DMA + scatter tail after the last gather, total (poller clock).
+ */
+typedef struct pulse_gs_engine pulse_gs_engine;
+PULSE_API pulse_status pulse_gs_engine_create(const pulse_shape* shape, int32_t n_workers,
+                                              int64_t max_blocks_per_call, int64_t staging_blocks,
+                                              pulse_gs_engine** engine);
+PULSE_API pulse_status pulse_gs_engine_destroy(pulse_gs_engine* engine);
+PULSE_API pulse_status pulse_gs_recall_submit(pulse_gs_engine* engine, const void* host_kv, const int64_t* blk_off,
+                                              int32_t B, const int32_t* sel_idx, const int32_t* sel_cnt,
+                                              int32_t k_max, int32_t* block_table, int32_t max_blocks,
+                                              const int32_t* free_slots, int32_t* free_head, int32_t n_free,
+                                              void* slot_pool, int32_t n_slots, pulse_recall_stats* stats,
+                                              int32_t* dev_status, void* ws, size_t ws_bytes, int64_t* seq,
+                                              pulse_stream_t stream);
+PULSE_API pulse_status pulse_gs_recall_poll(pulse_gs_engine* engine, int64_t seq, int32_t* done);
+PULSE_API pulse_status pulse_gs_recall_wait(pulse_gs_engine* engine, int64_t seq, int32_t timeout_ms);
+PULSE_API pulse_status pulse_gs_last_timing(pulse_gs_engine* engine, float* ms3);
 
 /*
  * a7. Sparse GQA decode attention over the selected blocks (the attention

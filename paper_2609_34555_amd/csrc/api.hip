@@ -65,6 +65,7 @@ const char* pulse_status_string(pulse_status s) {
         case PULSE_ERR_SELECT_OVERFLOW: return "PULSE_ERR_SELECT_OVERFLOW";
         case PULSE_ERR_HIP: return "PULSE_ERR_HIP";
         case PULSE_ERR_BAD_INDEX: return "PULSE_ERR_BAD_INDEX";
+        case PULSE_ERR_TIMEOUT: return "PULSE_ERR_TIMEOUT";
     }
     return "PULSE_ERR_UNKNOWN";
 }

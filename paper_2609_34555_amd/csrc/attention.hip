@@ -115,13 +115,14 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
     const size_t v_head = (size_t)Hkv * BS * kHeadDim + (size_t)h * kHeadDim * BS;
     const int tokens = ne * BS;
 
-    for (int t0 = 0; t0 < tokens; t0 += kChunkTokens) {
-        // --- K operand: MFMA row m = col maps to token 8*(col/4) + 4*sub + col%4
+    // K/V operand loads of one 32-token step starting at sequence token t0
+    // K: MFMA row m = col maps to token 8*(col/4) + 4*sub + col%4;
+    // V: lane group grp holds tokens 8*grp .. 8*grp+7 of channel col + 16*tile.
+    auto load_step = [&](int t0, vec (&ka)[2][4], vec (&vb)[8]) {
         const int ka_seq = t0 + 8 * (col >> 2);
         const int ka_e = ka_seq / BS;
         const int ka_slot = __shfl(my_slot, ka_e < ne ? ka_e : 0);
         const int ka_nv = __shfl(my_nv, ka_e < ne ? ka_e : 0);
-        vec ka[2][4];
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) {
             const int row = ka_seq % BS + 4 * sub + (col & 3);
@@ -130,19 +131,34 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
 #pragma unroll
             for (int kc = 0; kc < 4; ++kc) ka[sub][kc] = ok ? load_vec<DT>(kp + 32 * kc) : zero_vec<DT>();
         }
-        // --- V operand: lane group grp holds tokens 8*grp .. 8*grp+7 of channel col + 16*tile
+        const int pv_seq = t0 + 8 * grp;
+        const int pv_e = pv_seq / BS;
+        const int pv_slot = __shfl(my_slot, pv_e < ne ? pv_e : 0);
+        const bool pv_ok = pv_e < ne && pv_slot >= 0;
+        const uint16_t* vp = pool + (size_t)(pv_ok ? pv_slot : 0) * E + v_head + (size_t)col * BS + pv_seq % BS;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) vb[t] = pv_ok ? load_vec<DT>(vp + (size_t)16 * t * BS) : zero_vec<DT>();
+    };
+
+    // software pipeline: the loads of step i+1 are in flight while step i computes
+    vec ka_n[2][4], vb_n[8];
+    load_step(0, ka_n, vb_n);
+#pragma unroll 1
+    for (int t0 = 0; t0 < tokens; t0 += kChunkTokens) {
+        vec ka[2][4], vb[8];
+#pragma unroll
+        for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+            for (int kc = 0; kc < 4; ++kc) ka[sub][kc] = ka_n[sub][kc];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) vb[t] = vb_n[t];
+        if (t0 + kChunkTokens < tokens) load_step(t0 + kChunkTokens, ka_n, vb_n);
         const int pv_seq = t0 + 8 * grp;
         const int pv_e = pv_seq / BS;
         const int pv_slot = __shfl(my_slot, pv_e < ne ? pv_e : 0);
         const int pv_nv = __shfl(my_nv, pv_e < ne ? pv_e : 0);
         const int pv_row = pv_seq % BS;
         const bool pv_ok = pv_e < ne && pv_slot >= 0;
-        vec vb[8];
-        {
-            const uint16_t* vp = pool + (size_t)(pv_ok ? pv_slot : 0) * E + v_head + (size_t)col * BS + pv_row;
-#pragma unroll
-            for (int t = 0; t < 8; ++t) vb[t] = pv_ok ? load_vec<DT>(vp + (size_t)16 * t * BS) : zero_vec<DT>();
-        }
         // --- S^T = K . Q^T
         f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -318,7 +334,7 @@ AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
     // entries per 32-token step; a split covers >= 2 steps, <= 64 entries
     const int32_t step = bs >= kChunkTokens ? 1 : kChunkTokens / bs;
     const int64_t units = (int64_t)B * Hkv;
-    const int64_t target_waves = 4096;
+    const int64_t target_waves = 2048;  // one round at 2 resident waves per SIMD on 256 CUs
     int64_t want = units > 0 ? (target_waves + units - 1) / units : 1;
     int64_t min_entries = (bs >= 2 * kChunkTokens) ? 1 : (2 * kChunkTokens) / bs;
     int64_t max_split = (k_max + min_entries - 1) / min_entries;

@@ -120,13 +120,11 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
     const int head = gridDim.y > 1 ? (int)blockIdx.y : solo;
     digests += (size_t)blockIdx.y * total_blocks * 2 * kHeadDim;
     scores += (size_t)blockIdx.y * total_blocks;
-    for (int i = threadIdx.x; i <= B; i += 256) s_off[i] = blk_off[i];
-    __syncthreads();
     const int sub = threadIdx.x & 15;
     const int gi = threadIdx.x >> 4;
     const int c8 = sub * 8;
     const int64_t base = (int64_t)blockIdx.x * kScoreBlocksPerWg + gi;
-    // issue the digest loads of all four iterations before any q load
+    // digest loads first: their addresses do not depend on the request
     u32x4 dmn[4], dmx[4];
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
@@ -137,6 +135,8 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
             dmx[it] = dg[16 + sub];
         }
     }
+    for (int i = threadIdx.x; i <= B; i += 256) s_off[i] = blk_off[i];
+    __syncthreads();
     int cur_r = -1;
     int64_t r_lo = 0, r_hi = 0;
     uint32_t qp[G][4], qm[G][4];

@@ -167,6 +167,16 @@ class LayerState:
                               self.pool, w.n_slots, self.stats, self.dev_status, self.ws, self.ws_bytes,
                               stream=stream)
 
+    def recall_gs(self, engine, stream=None, wait=True, timeout_ms=20000):
+        """Recall through the CPU-gather / one-DMA / GPU-scatter engine (the paper's path)."""
+        w = self.w
+        seq = engine.submit(self.host_ptr, self.blk_off, w.B, self.sel_idx, self.sel_cnt, self.k_max, self.table,
+                            w.max_blocks, self.free_slots, self.free_head, int(w.free_slots.size), self.pool,
+                            w.n_slots, self.stats, self.dev_status, self.ws, self.ws_bytes, stream=stream)
+        if wait:
+            engine.wait(seq, timeout_ms)
+        return seq
+
     def attention(self, stream=None):
         w = self.w
         P.pulse_sparse_decode_attn(self.shape, self.q, self.pool, w.n_slots, self.table, w.max_blocks, self.sel_idx,

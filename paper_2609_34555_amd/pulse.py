@@ -22,6 +22,7 @@ PULSE_ERR_POOL_EXHAUSTED = 4
 PULSE_ERR_SELECT_OVERFLOW = 5
 PULSE_ERR_HIP = 6
 PULSE_ERR_BAD_INDEX = 7
+PULSE_ERR_TIMEOUT = 8
 PULSE_F16 = 0
 PULSE_BF16 = 1
 
@@ -30,7 +31,8 @@ EXPORTED = (
     "pulse_select_solohead", "pulse_recall_gather", "pulse_sparse_decode_attn", "pulse_decode_layer",
     "pulse_host_alloc", "pulse_host_free", "pulse_baseline_memcpy_units", "pulse_probe_host_read",
     "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms", "pulse_headwise_workspace_bytes",
-    "pulse_select_headwise",
+    "pulse_select_headwise", "pulse_gs_engine_create", "pulse_gs_engine_destroy", "pulse_gs_recall_submit",
+    "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing",
 )
 
 
@@ -99,6 +101,13 @@ def lib():
             "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
             "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
                                                      _P, _P, _P, _P, _P, SZ, _P]),
+            "pulse_gs_engine_create": (ctypes.c_int, [SP, I32, I64, I64, ctypes.POINTER(ctypes.c_void_p)]),
+            "pulse_gs_engine_destroy": (ctypes.c_int, [_P]),
+            "pulse_gs_recall_submit": (ctypes.c_int, [_P, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
+                                                      _P, _P, SZ, ctypes.POINTER(ctypes.c_int64), _P]),
+            "pulse_gs_recall_poll": (ctypes.c_int, [_P, I64, ctypes.POINTER(ctypes.c_int32)]),
+            "pulse_gs_recall_wait": (ctypes.c_int, [_P, I64, I32]),
+            "pulse_gs_last_timing": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_float)]),
             "pulse_events_create": (ctypes.c_int, [I32, _P]),
             "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
             "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
@@ -230,6 +239,44 @@ def pulse_baseline_memcpy_units(host_kv, pool, src_units, dst_units, n, unit_byt
 def pulse_probe_host_read(host_src, dev_dst, nbytes, stream=None, check=True):
     st = lib().pulse_probe_host_read(_ptr(host_src), _ptr(dev_dst), nbytes, _stream(stream))
     return _check(st, "pulse_probe_host_read", check)
+
+
+class GatherScatterEngine:
+    """Handle of a pulse_gs_engine (the paper's CPU-gather / one-DMA / GPU-scatter path)."""
+
+    def __init__(self, shape: pulse_shape, n_workers: int, max_blocks_per_call: int, staging_blocks: int):
+        h = ctypes.c_void_p()
+        _check(lib().pulse_gs_engine_create(ctypes.byref(shape), n_workers, max_blocks_per_call, staging_blocks,
+                                            ctypes.byref(h)), "pulse_gs_engine_create", True)
+        self.handle = h.value
+
+    def submit(self, host_kv, blk_off, B, sel_idx, sel_cnt, k_max, block_table, max_blocks, free_slots, free_head,
+               n_free, slot_pool, n_slots, stats, dev_status, ws, ws_bytes, stream=None) -> int:
+        seq = ctypes.c_int64()
+        _check(lib().pulse_gs_recall_submit(self.handle, _ptr(host_kv), _ptr(blk_off), B, _ptr(sel_idx),
+                                            _ptr(sel_cnt), k_max, _ptr(block_table), max_blocks, _ptr(free_slots),
+                                            _ptr(free_head), n_free, _ptr(slot_pool), n_slots, _ptr(stats),
+                                            _ptr(dev_status), _ptr(ws), ws_bytes, ctypes.byref(seq),
+                                            _stream(stream)), "pulse_gs_recall_submit", True)
+        return seq.value
+
+    def poll(self, seq: int) -> bool:
+        done = ctypes.c_int32()
+        _check(lib().pulse_gs_recall_poll(self.handle, seq, ctypes.byref(done)), "pulse_gs_recall_poll", True)
+        return bool(done.value)
+
+    def wait(self, seq: int, timeout_ms: int = 10000):
+        return _check(lib().pulse_gs_recall_wait(self.handle, seq, timeout_ms), "pulse_gs_recall_wait", True)
+
+    def last_timing(self):
+        ms = (ctypes.c_float * 3)()
+        _check(lib().pulse_gs_last_timing(self.handle, ms), "pulse_gs_last_timing", True)
+        return {"gather_ms": ms[0], "dma_scatter_tail_ms": ms[1], "total_ms": ms[2]}
+
+    def destroy(self):
+        if self.handle:
+            lib().pulse_gs_engine_destroy(self.handle)
+            self.handle = None
 
 
 class EventSet:

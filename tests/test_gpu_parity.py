@@ -335,3 +335,50 @@ def test_multilayer_overlapped_matches_chained_and_oracle():
         st = ml.layers[i]
         res = full_check(st.w, st, chained=True)
         say(f"  layer {i}: stats={res['stats']} attn_err={res['attn_err']}")
+
+
+# ------------------------------------------------------------------ the paper's gather-scatter engine
+
+@pytest.mark.parametrize("cid,kw", [(2, dict(ctx_scale=1 / 8)), (5, dict(ctx_scale=1 / 16)),
+                                    (3, dict(ctx_scale=1 / 16, batch=5))])
+def test_gather_scatter_engine_matches_oracle(cid, kw):
+    """CPU gather -> one DMA -> GPU scatter, submitted through the host-visible mailbox:
+    table, free head, stats and every pool byte as the oracle; attention after completion."""
+    spec, s = W.preset(cid, **kw)
+    w, st = build(spec, s)
+    eng = P.GatherScatterEngine(st.shape, n_workers=4, max_blocks_per_call=w.B * st.k_max, staging_blocks=64)
+    try:
+        for rep in range(2):  # the second call reuses the engine (sequence numbers advance)
+            st.reset()
+            st.select()
+            seq = st.recall_gs(eng, wait=False)
+            with pytest.raises(P.PulseError):  # one call in flight per engine
+                st.recall_gs(eng, wait=False)
+            eng.wait(seq, 20000)
+            assert eng.poll(seq)
+            st.attention()
+            torch.cuda.synchronize()
+            assert st.status() == 0
+            res = full_check(w, st, run=False)
+            say(f"  rep {rep}: stats={res['stats']} timing={eng.last_timing()}")
+    finally:
+        eng.destroy()
+
+
+def test_gather_scatter_engine_pool_exhaustion():
+    spec, s = W.custom("gsx", [3000, 3000], Hq=32, Hkv=8, bs=16, k_mid=40, n_sink=1, n_local=8,
+                       resident_frac=0.05, n_free_override=10)
+    w, st = build(spec, s)
+    eng = P.GatherScatterEngine(st.shape, n_workers=2, max_blocks_per_call=w.B * st.k_max, staging_blocks=16)
+    try:
+        st.select()
+        pool0 = st.pool.clone()
+        seq = st.recall_gs(eng, wait=False)
+        with pytest.raises(P.PulseError) as e:
+            eng.wait(seq, 20000)
+        assert e.value.status == P.PULSE_ERR_POOL_EXHAUSTED
+        torch.cuda.synchronize()
+        assert st.status() == P.PULSE_ERR_POOL_EXHAUSTED
+        assert torch.equal(st.table, st.table0) and int(st.free_head.item()) == 0 and torch.equal(st.pool, pool0)
+    finally:
+        eng.destroy()
