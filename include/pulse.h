@@ -316,6 +316,45 @@ typedef struct {
  */
 PULSE_API pulse_status pulse_decode_layer(const pulse_layer_args* args, pulse_stream_t stream);
 
+/* ---- IO-Adaptive Offloading Admission (Sec. 4.3; host side) ---- */
+
+typedef struct {
+    int64_t gpu_budget_bytes;    /* GPU memory available to newly admitted requests */
+    int64_t kv_bytes_per_token;  /* KV bytes of one token over all layers and KV heads */
+    int64_t offload_tokens;      /* GPU-resident hot budget of an offloaded request (tokens) */
+    int64_t offload_extra_bytes; /* further GPU bytes per offloaded request (digests, tables) */
+    int32_t running_normal;      /* requests already in the normal batch */
+    int32_t running_offload;     /* requests already in the offload batch */
+    const double* grid_bo;       /* profiled offload-batch sizes, ascending [n_bo] */
+    int32_t n_bo;
+    const double* grid_bn;       /* profiled normal-batch sizes, ascending [n_bn] */
+    int32_t n_bn;
+    const double* grid_m;        /* overlap depth m at (grid_bo[i], grid_bn[j]): [n_bo][n_bn] */
+} pulse_ioaa_params;
+
+/*
+ * Overlap depth m(B_o, B_n): bilinear interpolation of the profiled grid,
+ * clamped at its edges (Sec. 4.3.2: m = ceil(t_io / t_layer), profiled on a
+ * (B_o, B_n) grid and interpolated from the nearest points).  NaN on a bad grid.
+ */
+PULSE_API double pulse_overlap_depth(const pulse_ioaa_params* params, double b_o, double b_n);
+
+/*
+ * Admission of n waiting requests (Sec. 4.3.1): maximise Eq. 1,
+ *   thr = m/(m+1) * B_n + 1/(m+1) * B_o   (thr = B_n when B_o = 0),
+ * over assignments of each request to the normal batch (its whole KV cache,
+ * lengths[i] * kv_bytes_per_token bytes) or the offload batch (offload_tokens
+ * * kv_bytes_per_token + offload_extra_bytes), by a depth-first binary-tree
+ * search over the requests longest first with two prunes: the memory budget,
+ * and no offloading after a longer request went to the normal batch.  A request
+ * that fits neither batch ends its path (it and all shorter ones wait).
+ *   assign[i] = 0 wait, 1 normal, 2 offload (host array); *throughput = Eq. 1
+ *   at the chosen assignment; *nodes_visited (optional) = search nodes.
+ * Host-only; no GPU work.
+ */
+PULSE_API pulse_status pulse_ioaa_plan(const pulse_ioaa_params* params, const int64_t* lengths, int32_t n,
+                                       int8_t* assign, double* throughput, int64_t* nodes_visited);
+
 /* ---- measurement helpers (host side; not part of the compute path) ---- */
 
 /*

@@ -32,7 +32,8 @@ EXPORTED = (
     "pulse_host_alloc", "pulse_host_free", "pulse_baseline_memcpy_units", "pulse_probe_host_read",
     "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms", "pulse_headwise_workspace_bytes",
     "pulse_select_headwise", "pulse_gs_engine_create", "pulse_gs_engine_destroy", "pulse_gs_recall_submit",
-    "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing",
+    "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing", "pulse_overlap_depth",
+    "pulse_ioaa_plan",
 )
 
 
@@ -52,6 +53,14 @@ class pulse_recall_stats(ctypes.Structure):
 
 
 _P = ctypes.c_void_p
+
+
+class pulse_ioaa_params(ctypes.Structure):
+    _fields_ = [("gpu_budget_bytes", ctypes.c_int64), ("kv_bytes_per_token", ctypes.c_int64),
+                ("offload_tokens", ctypes.c_int64), ("offload_extra_bytes", ctypes.c_int64),
+                ("running_normal", ctypes.c_int32), ("running_offload", ctypes.c_int32),
+                ("grid_bo", ctypes.c_void_p), ("n_bo", ctypes.c_int32), ("grid_bn", ctypes.c_void_p),
+                ("n_bn", ctypes.c_int32), ("grid_m", ctypes.c_void_p)]
 
 
 class pulse_layer_args(ctypes.Structure):
@@ -108,6 +117,10 @@ def lib():
             "pulse_gs_recall_poll": (ctypes.c_int, [_P, I64, ctypes.POINTER(ctypes.c_int32)]),
             "pulse_gs_recall_wait": (ctypes.c_int, [_P, I64, I32]),
             "pulse_gs_last_timing": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_float)]),
+            "pulse_overlap_depth": (ctypes.c_double, [ctypes.POINTER(pulse_ioaa_params), ctypes.c_double,
+                                                      ctypes.c_double]),
+            "pulse_ioaa_plan": (ctypes.c_int, [ctypes.POINTER(pulse_ioaa_params), _P, I32, _P,
+                                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
             "pulse_events_create": (ctypes.c_int, [I32, _P]),
             "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
             "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
@@ -239,6 +252,39 @@ def pulse_baseline_memcpy_units(host_kv, pool, src_units, dst_units, n, unit_byt
 def pulse_probe_host_read(host_src, dev_dst, nbytes, stream=None, check=True):
     st = lib().pulse_probe_host_read(_ptr(host_src), _ptr(dev_dst), nbytes, _stream(stream))
     return _check(st, "pulse_probe_host_read", check)
+
+
+def make_ioaa_params(gpu_budget_bytes, kv_bytes_per_token, offload_tokens, offload_extra_bytes, running_normal,
+                     running_offload, grid_bo, grid_bn, grid_m):
+    """pulse_ioaa_params holding references to float64 numpy grids (kept on the struct)."""
+    import numpy as np
+
+    bo = np.ascontiguousarray(grid_bo, dtype=np.float64)
+    bn = np.ascontiguousarray(grid_bn, dtype=np.float64)
+    m = np.ascontiguousarray(grid_m, dtype=np.float64).reshape(bo.size, bn.size)
+    p = pulse_ioaa_params(int(gpu_budget_bytes), int(kv_bytes_per_token), int(offload_tokens),
+                          int(offload_extra_bytes), int(running_normal), int(running_offload), bo.ctypes.data,
+                          bo.size, bn.ctypes.data, bn.size, m.ctypes.data)
+    p._keep = (bo, bn, m)
+    return p
+
+
+def pulse_overlap_depth(params: pulse_ioaa_params, b_o: float, b_n: float) -> float:
+    return lib().pulse_overlap_depth(ctypes.byref(params), float(b_o), float(b_n))
+
+
+def pulse_ioaa_plan(params: pulse_ioaa_params, lengths):
+    """Returns (assign int8 [n]: 0 wait / 1 normal / 2 offload, throughput, nodes_visited)."""
+    import numpy as np
+
+    L = np.ascontiguousarray(lengths, dtype=np.int64)
+    assign = np.zeros(L.size, np.int8)
+    thr = ctypes.c_double()
+    nodes = ctypes.c_int64()
+    _check(lib().pulse_ioaa_plan(ctypes.byref(params), L.ctypes.data if L.size else None, L.size,
+                                 assign.ctypes.data if L.size else None, ctypes.byref(thr), ctypes.byref(nodes)),
+           "pulse_ioaa_plan", True)
+    return assign, thr.value, nodes.value
 
 
 class GatherScatterEngine:

@@ -1,0 +1,124 @@
+"""IO-Adaptive Offloading Admission (Sec. 4.3): oracle pins and library parity (CPU)."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ioaa as OI
+from paper_2609_34555_amd import pulse as P
+
+
+# ------------------------------------------------------------------ oracle pins
+
+def test_eq1_closed_forms():
+    assert OI.throughput(6, 2, 1.0) == pytest.approx(4.0)     # m = 1: mean of the two batches
+    assert OI.throughput(8, 4, 3.0) == pytest.approx(7.0)     # 3/4 * 8 + 1/4 * 4
+    assert OI.throughput(5, 0, 7.0) == 5.0                    # no offload batch: the normal batch alone
+    # the normal batch always weighs more (m >= 1): moving a request to the normal batch never hurts
+    for m in (1.0, 2.5, 9.0):
+        assert OI.throughput(3, 2, m) >= OI.throughput(2, 3, m)
+
+
+def test_interpolation_reproduces_planar_grid_and_clamps():
+    bo = [1.0, 2.0, 4.0, 8.0]
+    bn = [1.0, 16.0, 64.0]
+    plane = lambda x, y: 1.0 + 0.5 * x + 0.01 * y  # noqa: E731  bilinear interpolation is exact on planes
+    m = [[plane(x, y) for y in bn] for x in bo]
+    for x, y in [(1.0, 1.0), (3.0, 10.0), (7.5, 63.0), (2.0, 16.0)]:
+        assert OI.overlap_depth(bo, bn, m, x, y) == pytest.approx(plane(x, y))
+    assert OI.overlap_depth(bo, bn, m, 100.0, 1000.0) == pytest.approx(plane(8.0, 64.0))
+    assert OI.overlap_depth(bo, bn, m, 0.0, 0.0) == pytest.approx(plane(1.0, 1.0))
+
+
+def test_hand_worked_admission():
+    """Budget 100 B, 1 B/token, hot budget 10 tokens, m = 3: lengths 60, 50, 40, 5.
+    Paths (longest first, normal branch first): N60 -> 1.0; O60 N50 N40 -> 1.75;
+    O60 O50 N40 N5 -> 0.75*2 + 0.25*2 = 2.0 (best); O60 O50 O40 N5 -> 1.5; all offloaded -> 1.0."""
+    assign, thr = OI.best_assignment([60, 50, 40, 5], 100, 1, 10, 0, 0, 0, [1.0], [1.0], [[3.0]])
+    assert assign == [2, 2, 1, 1] and thr == pytest.approx(2.0)
+
+
+def test_unconstrained_memory_admits_everything_normal():
+    assign, thr = OI.best_assignment([9, 7, 3], 10 ** 9, 1, 2, 0, 0, 0, [1.0, 10.0], [1.0, 10.0], [[1.0, 2.0],
+                                                                                                [3.0, 4.0]])
+    assert assign == [1, 1, 1] and thr == 3.0
+
+
+# ------------------------------------------------------------------ library vs oracle
+
+def _params(budget, kvb, hot, extra, rn, ro, bo, bn, m):
+    return P.make_ioaa_params(budget, kvb, hot, extra, rn, ro, bo, bn, m)
+
+
+def test_library_interpolation_matches_oracle():
+    rng = np.random.default_rng(5)
+    bo = np.cumsum(rng.uniform(0.5, 3, 5))
+    bn = np.cumsum(rng.uniform(1, 8, 4))
+    m = rng.uniform(1, 6, (5, 4))
+    p = _params(1, 1, 1, 0, 0, 0, bo, bn, m)
+    for _ in range(200):
+        x, y = rng.uniform(-1, bo[-1] + 2), rng.uniform(-1, bn[-1] + 5)
+        assert P.pulse_overlap_depth(p, x, y) == pytest.approx(OI.overlap_depth(bo, bn, m, x, y), rel=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_library_search_equals_exhaustive_oracle(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(0, 8))
+    lengths = [int(x) for x in rng.integers(1, 200, n)]
+    budget = int(rng.integers(20, 600))
+    hot = int(rng.integers(1, 30))
+    extra = int(rng.integers(0, 5))
+    rn, ro = int(rng.integers(0, 4)), int(rng.integers(0, 3))
+    bo = np.cumsum(rng.uniform(0.5, 3, 4))
+    bn = np.cumsum(rng.uniform(1, 5, 3))
+    m = rng.uniform(1, 6, (4, 3))
+    want, want_thr = OI.best_assignment(lengths, budget, 1, hot, extra, rn, ro, bo, bn, m)
+    p = _params(budget, 1, hot, extra, rn, ro, bo, bn, m)
+    got, thr, nodes = P.pulse_ioaa_plan(p, lengths)
+    assert thr == pytest.approx(want_thr, rel=1e-12, abs=1e-12)
+    # the library's assignment is admissible and reaches that throughput
+    order = sorted(range(n), key=lambda i: (-lengths[i], i))
+    mem, seen_normal, b_n, b_o = 0, False, rn, ro
+    decided = [got[i] for i in order]
+    k = next((t for t, a in enumerate(decided) if a == 0), n)
+    assert all(a == 0 for a in decided[k:])
+    for t in range(k):
+        L = lengths[order[t]]
+        if decided[t] == 1:
+            mem += L
+            seen_normal = True
+            b_n += 1
+        else:
+            assert not seen_normal
+            mem += hot + extra
+            b_o += 1
+        assert mem <= budget
+    assert OI.throughput(b_n, b_o, OI.overlap_depth(bo, bn, m, b_o, b_n)) == pytest.approx(thr, rel=1e-12)
+    assert nodes >= 1
+
+
+def test_pruned_search_is_small_under_memory_pressure():
+    """30 waiting requests of lognormal lengths, GPU room for a few long ones: the two prunes
+    keep the walk to a few nodes per request (about 18 on average here; the paper reports
+    3.16 on average for 30 waiting requests on its own serving trace, Sec. 4.3.1)."""
+    rng = np.random.default_rng(0)
+    bo = [1.0, 4.0, 16.0, 64.0]
+    bn = [1.0, 16.0, 64.0]
+    m = [[1.0, 1.0, 1.0], [1.5, 1.3, 1.2], [3.0, 2.5, 2.2], [9.0, 8.0, 7.0]]
+    counts = []
+    for _ in range(50):
+        lengths = np.clip(rng.lognormal(np.log(16384), 1.0, 30), 256, 262144).astype(np.int64)
+        budget = int(rng.uniform(0.5, 3.0) * 16384 * 160 * 1024)  # room for a few long requests
+        p = _params(budget, 160 * 1024, 2048, 1 << 20, 8, 4, bo, bn, m)
+        _, _, nodes = P.pulse_ioaa_plan(p, lengths)
+        counts.append(nodes)
+    assert np.mean(counts) < 2 * 30  # far below the 2^30 leaves of the unpruned tree
+    assert max(counts) < 4 * 30
+
+
+def test_validation():
+    p = _params(100, 1, 10, 0, 0, 0, [2.0, 1.0], [1.0], [[1.0], [2.0]])  # descending grid
+    with pytest.raises(P.PulseError):
+        P.pulse_ioaa_plan(p, [5, 6])
+    assert math.isnan(P.pulse_overlap_depth(P.pulse_ioaa_params(), 1.0, 1.0))
