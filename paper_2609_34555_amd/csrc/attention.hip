@@ -20,19 +20,26 @@
 // single bf16 rounding.  Softmax is online per 32-token step in the log2
 // domain.
 //
-// Merging the splits: a workgroup holds 4 waves = 4 consecutive splits of one
-// (r, h); they merge through LDS.  With one workgroup per (r, h) it writes the
-// result directly.  Otherwise each workgroup writes one partial (m, l, O) to
-// the workspace and a combine kernel merges those few partials with 256
-// threads per (r, h) and independent loads.  (Merging in the last workgroup
+// Merging the splits: a workgroup holds W waves = W consecutive splits of one
+// (r, h) (W = 8 for G <= 8, else 4); they merge through LDS.  With one
+// workgroup per (r, h) it writes the result directly.  Otherwise each workgroup writes one partial (m, l, O) to
+// the workspace and a combine kernel merges those few partials, one thread
+// per output element, with independent loads.  (Merging in the last workgroup
 // to finish would need a device-scope release fence per workgroup, which on
 // gfx950 writes back the XCD's L2 and costs more than the extra launch.)
 #include "pulse_internal.h"
 
 namespace pulse {
 
-constexpr int kAttnWaves = 4;
-constexpr int kAttnThreads = kAttnWaves * kWave;
+#ifndef PULSE_ATTN_TARGET_WAVES
+#define PULSE_ATTN_TARGET_WAVES 2048
+#endif
+constexpr int kCombineThreads = kHeadDim;
+
+// Waves per workgroup: 8 while the LDS merge buffer (waves x G x 128 floats)
+// stays within 32 KiB, else 4.  Fewer, wider workgroups leave fewer partials
+// for the combine kernel.
+inline int attn_waves(int G) { return G <= 8 ? 8 : 4; }
 
 template <int DT>
 struct Mfma;
@@ -215,19 +222,20 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
     l_run += __shfl_xor(l_run, 32);
 }
 
-// grid = (workgroups per (r, h), Hkv, B); 4 waves per workgroup, wave w owns
-// split 4*blockIdx.x + w of eps entries.  Dynamic LDS: O [4][G][128] floats
-// then (m, l) [4][G] float2.
-template <int DT, int BS>
-__global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
+// grid = (workgroups per (r, h), Hkv, B); W waves per workgroup, wave w owns
+// split W*blockIdx.x + w of eps entries.  Dynamic LDS: O [W][G][128] floats
+// then (m, l) [W][G] float2.
+template <int DT, int BS, int W>
+__global__ __launch_bounds__(W * kWave) void attn_splitk_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ pool, int32_t n_slots,
     const int32_t* __restrict__ table, int32_t max_blocks, const int32_t* __restrict__ sel_idx,
     const int32_t* __restrict__ sel_cnt, int32_t k_max, const int32_t* __restrict__ ctx_len, int32_t Hq,
     int32_t Hkv, int32_t G, int32_t eps, int32_t n_wg, float scale_log2, float* __restrict__ ws_o,
     float2* __restrict__ ws_ml, float* __restrict__ out, float* __restrict__ lse, int32_t* status) {
     extern __shared__ float smem[];
-    float* s_o = smem;                                                           // [4][G][128]
-    float2* s_ml = reinterpret_cast<float2*>(smem + kAttnWaves * G * kHeadDim);  // [4][G]
+    constexpr int kThreads = W * kWave;
+    float* s_o = smem;                                                           // [W][G][128]
+    float2* s_ml = reinterpret_cast<float2*>(smem + W * G * kHeadDim);  // [W][G]
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
     const int wg = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
@@ -240,15 +248,15 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
         cnt = 0;
     }
     const int ns = (cnt + eps - 1) / eps;                // non-empty splits of (r, h)
-    const int nwg = (ns + kAttnWaves - 1) / kAttnWaves;  // workgroups with work
+    const int nwg = (ns + W - 1) / W;  // workgroups with work
     if (wg >= nwg) {
         if (cnt == 0 && wg == 0) {  // empty selection: out = 0, lse = -inf
-            for (int i = tid; i < G * kHeadDim; i += kAttnThreads) out_rh[i] = 0.f;
+            for (int i = tid; i < G * kHeadDim; i += kThreads) out_rh[i] = 0.f;
             if (lse_rh && tid < G) lse_rh[tid] = -INFINITY;
         }
         return;
     }
-    const int s = wg * kAttnWaves + wave;
+    const int s = wg * W + wave;
     const int e0 = s * eps;
     const int ne = min(e0 + eps, cnt) - e0;
     float m_run, l_run;
@@ -267,17 +275,17 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
         }
     }
     __syncthreads();
-    // merge the 4 waves: thread handles outputs (g, c) = (idx / 128, idx % 128)
+    // merge the W waves: thread handles outputs (g, c) = (idx / 128, idx % 128)
     const size_t unit = ((size_t)r * Hkv + h) * n_wg + wg;
-    for (int idx = tid; idx < G * kHeadDim; idx += kAttnThreads) {
+    for (int idx = tid; idx < G * kHeadDim; idx += kThreads) {
         const int g = idx / kHeadDim, c = idx % kHeadDim;
         float Mx = -INFINITY;
 #pragma unroll
-        for (int w = 0; w < kAttnWaves; ++w) Mx = fmaxf(Mx, s_ml[w * G + g].x);
+        for (int w = 0; w < W; ++w) Mx = fmaxf(Mx, s_ml[w * G + g].x);
         float L = 0.f, a = 0.f;
         if (Mx != -INFINITY) {
 #pragma unroll
-            for (int w = 0; w < kAttnWaves; ++w) {
+            for (int w = 0; w < W; ++w) {
                 const float2 ml = s_ml[w * G + g];
                 const float wt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - Mx);
                 L += ml.y * wt;
@@ -294,47 +302,77 @@ __global__ __launch_bounds__(kAttnThreads) void attn_splitk_kernel(
     }
 }
 
-// Merge the workgroup partials of one (request, KV head): grid = (Hkv, B),
-// 256 threads, thread owns outputs (g, c) = (idx / 128, idx % 128).  Requests
-// whose selection fits one workgroup were finished by the attention kernel.
-__global__ __launch_bounds__(kAttnThreads) void attn_combine_kernel(
+// Merge the workgroup partials of one (request, KV head, query head):
+// grid = (G, Hkv, B), 128 threads, thread c owns output channel c.  Partials
+// are read 8 at a time (16 independent loads per thread) and merged online.
+// Requests whose selection fits one workgroup were finished by the attention
+// kernel.
+__global__ __launch_bounds__(kCombineThreads) void attn_combine_kernel(
     const float* __restrict__ ws_o, const float2* __restrict__ ws_ml, const int32_t* __restrict__ sel_cnt,
-    int32_t k_max, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps, int32_t n_wg, float* __restrict__ out,
-    float* __restrict__ lse) {
-    const int tid = threadIdx.x, h = blockIdx.x, r = blockIdx.y;
+    int32_t k_max, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps, int32_t n_wg, int32_t waves,
+    float* __restrict__ out, float* __restrict__ lse) {
+    const int c = threadIdx.x, g = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+    const size_t u0 = ((size_t)r * Hkv + h) * n_wg;
+    const float2* ml = ws_ml + u0 * G + g;                  // stride G
+    const float* po = ws_o + (u0 * G + g) * kHeadDim + c;   // stride G * 128
+    // the first 8 partials are loaded before the request's workgroup count is
+    // known (n_wg bounds it); entries past that count are discarded below
+    float2 mlv[8];
+    float ov[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        mlv[i] = i < n_wg ? ml[(size_t)i * G] : make_float2(-INFINITY, 0.f);
+        ov[i] = i < n_wg ? po[(size_t)i * G * kHeadDim] : 0.f;
+    }
     int32_t cnt = sel_cnt[r];
     if (cnt < 0 || cnt > k_max) cnt = 0;
     const int ns = (cnt + eps - 1) / eps;
-    const int nwg = (ns + kAttnWaves - 1) / kAttnWaves;
+    const int nwg = (ns + waves - 1) / waves;
     if (nwg <= 1) return;
-    float* out_rh = out + ((size_t)r * Hq + (size_t)h * G) * kHeadDim;
-    float* lse_rh = lse ? lse + (size_t)r * Hq + (size_t)h * G : nullptr;
-    const size_t u0 = ((size_t)r * Hkv + h) * n_wg;
-    for (int idx = tid; idx < G * kHeadDim; idx += kAttnThreads) {
-        const int g = idx / kHeadDim;
-        float Mx = -INFINITY;
-        for (int w = 0; w < nwg; ++w) Mx = fmaxf(Mx, ws_ml[(u0 + w) * G + g].x);
-        float L = 0.f, a = 0.f;
-        if (Mx != -INFINITY) {
-#pragma unroll 8
-            for (int w = 0; w < nwg; ++w) {
-                const float2 ml = ws_ml[(u0 + w) * G + g];
-                const float wt = ml.x == -INFINITY ? 0.f : exp2f(ml.x - Mx);
-                L += ml.y * wt;
-                a += ws_o[(u0 + w) * G * kHeadDim + idx] * wt;
+    float m_run = -INFINITY, L = 0.f, a = 0.f;
+    for (int w0 = 0; w0 < nwg; w0 += 8) {
+        if (w0 > 0) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const bool ok = w0 + i < nwg;
+                mlv[i] = ok ? ml[(size_t)(w0 + i) * G] : make_float2(-INFINITY, 0.f);
+                ov[i] = ok ? po[(size_t)(w0 + i) * G * kHeadDim] : 0.f;
             }
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+                if (i >= nwg) {  // not written by this call
+                    mlv[i] = make_float2(-INFINITY, 0.f);
+                    ov[i] = 0.f;
+                }
         }
-        out_rh[idx] = Mx == -INFINITY ? 0.f : a / L;
-        if (lse_rh && idx % kHeadDim == 0)
-            lse_rh[g] = Mx == -INFINITY ? -INFINITY : (Mx + log2f(L)) * 0.69314718055994531f;
+        float cm = m_run;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) cm = fmaxf(cm, mlv[i].x);
+        if (cm == -INFINITY) continue;
+        const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - cm);
+        L *= alpha;
+        a *= alpha;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float wt = mlv[i].x == -INFINITY ? 0.f : exp2f(mlv[i].x - cm);
+            L += mlv[i].y * wt;
+            a += ov[i] * wt;
+        }
+        m_run = cm;
     }
+    float* out_rg = out + ((size_t)r * Hq + (size_t)h * G + g) * kHeadDim;
+    out_rg[c] = m_run == -INFINITY ? 0.f : a / L;
+    if (lse && c == 0)
+        lse[(size_t)r * Hq + (size_t)h * G + g] =
+            m_run == -INFINITY ? -INFINITY : (m_run + log2f(L)) * 0.69314718055994531f;
 }
 
 AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
     // entries per 32-token step; a split covers >= 2 steps, <= 64 entries
     const int32_t step = bs >= kChunkTokens ? 1 : kChunkTokens / bs;
     const int64_t units = (int64_t)B * Hkv;
-    const int64_t target_waves = 2048;  // one round at 2 resident waves per SIMD on 256 CUs
+    const int64_t target_waves = PULSE_ATTN_TARGET_WAVES;  // one round at 2 resident waves per SIMD on 256 CUs
     int64_t want = units > 0 ? (target_waves + units - 1) / units : 1;
     int64_t min_entries = (bs >= 2 * kChunkTokens) ? 1 : (2 * kChunkTokens) / bs;
     int64_t max_split = (k_max + min_entries - 1) / min_entries;
@@ -350,13 +388,13 @@ AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
     return p;
 }
 
-template <int DT, int BS>
+template <int DT, int BS, int W>
 static void launch_attn_t(dim3 grid, size_t lds, hipStream_t st, const void* q, const void* pool, int32_t n_slots,
                           const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
                           int32_t k_max, const int32_t* ctx_len, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps,
                           int32_t n_wg, float scale_log2, float* ws_o, float2* ws_ml, float* out, float* lse,
                           int32_t* status) {
-    hipLaunchKernelGGL((attn_splitk_kernel<DT, BS>), grid, dim3(kAttnThreads), lds, st, (const uint16_t*)q,
+    hipLaunchKernelGGL((attn_splitk_kernel<DT, BS, W>), grid, dim3(W * kWave), lds, st, (const uint16_t*)q,
                        (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, Hkv,
                        G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse, status);
 }
@@ -368,27 +406,31 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
     if (B == 0) return hipSuccess;
     const int32_t Hkv = s.num_kv_heads, Hq = s.num_q_heads, G = Hq / Hkv;
     const AttnPlan p = attn_plan(B, Hkv, k_max, s.block_size);
-    const int32_t n_wg = (p.n_split + kAttnWaves - 1) / kAttnWaves;
+    const int W = attn_waves(G);
+    const int32_t n_wg = (p.n_split + W - 1) / W;
     dim3 grid((unsigned)n_wg, (unsigned)Hkv, (unsigned)B);
-    const size_t lds = sizeof(float) * kAttnWaves * G * kHeadDim + sizeof(float2) * kAttnWaves * G;
+    const size_t lds = sizeof(float) * W * G * kHeadDim + sizeof(float2) * W * G;
     const float scale_log2 = sm_scale * 1.4426950408889634f;
-#define PULSE_ATTN(DT, BS)                                                                                        \
-    launch_attn_t<DT, BS>(grid, lds, st, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, \
-                          Hkv, G, p.entries_per_split, n_wg, scale_log2, ws_o, ws_ml, out, lse, status)
+#define PULSE_ATTN(DT, BS, W)                                                                                        \
+    launch_attn_t<DT, BS, W>(grid, lds, st, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len,   \
+                             Hq, Hkv, G, p.entries_per_split, n_wg, scale_log2, ws_o, ws_ml, out, lse, status)
+#define PULSE_ATTN_W(DT, BS) \
+    if (W == 8) PULSE_ATTN(DT, BS, 8); else PULSE_ATTN(DT, BS, 4)
     if (s.dtype == PULSE_BF16) {
-        if (s.block_size == 16) PULSE_ATTN(PULSE_BF16, 16);
-        else if (s.block_size == 32) PULSE_ATTN(PULSE_BF16, 32);
-        else PULSE_ATTN(PULSE_BF16, 64);
+        if (s.block_size == 16) PULSE_ATTN_W(PULSE_BF16, 16);
+        else if (s.block_size == 32) PULSE_ATTN_W(PULSE_BF16, 32);
+        else PULSE_ATTN_W(PULSE_BF16, 64);
     } else {
-        if (s.block_size == 16) PULSE_ATTN(PULSE_F16, 16);
-        else if (s.block_size == 32) PULSE_ATTN(PULSE_F16, 32);
-        else PULSE_ATTN(PULSE_F16, 64);
+        if (s.block_size == 16) PULSE_ATTN_W(PULSE_F16, 16);
+        else if (s.block_size == 32) PULSE_ATTN_W(PULSE_F16, 32);
+        else PULSE_ATTN_W(PULSE_F16, 64);
     }
+#undef PULSE_ATTN_W
 #undef PULSE_ATTN
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || n_wg <= 1) return e;
-    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)Hkv, (unsigned)B), dim3(kAttnThreads), 0, st, ws_o, ws_ml,
-                       sel_cnt, k_max, Hq, Hkv, G, p.entries_per_split, n_wg, out, lse);
+    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)G, (unsigned)Hkv, (unsigned)B), dim3(kCombineThreads), 0,
+                       st, ws_o, ws_ml, sel_cnt, k_max, Hq, Hkv, G, p.entries_per_split, n_wg, W, out, lse);
     return hipGetLastError();
 }
 

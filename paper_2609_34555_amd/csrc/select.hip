@@ -6,14 +6,17 @@
 // middle blocks of highest score are chosen, equal scores in ascending
 // block order; the set is emitted ascending.  One 1024-thread workgroup per
 // request:
-//   1. radix select (8-bit passes over an LDS copy of the keys, starting at the
-//      highest byte in which the keys differ) of the k'-th largest
-//      order-preserving key of the fp32 scores -> threshold T and the number
-//      need_eq of keys equal to T that are taken;
-//   2. one ordered pass over the blocks in tiles of 1024 with wave ballots and
-//      a cross-wave LDS scan: block j is chosen if key > T, or key == T and
-//      fewer than need_eq equal keys precede it -- this is exactly the
-//      lowest-index tie rule.
+//   1. radix select (8-bit passes over an LDS copy of the keys, on the offsets
+//      key - min key, from the highest bit of the key range down) of the k'-th
+//      largest order-preserving key of the fp32 scores.  It ends at the first
+//      pass whose bucket holding the k'-th offset is taken whole, leaving a
+//      threshold T on the decided high bits (mask M) and the number need_eq of
+//      offsets with those bits equal to T that are taken;
+//   2. one ordered pass over super-tiles of 8192 blocks, thread t owning 8
+//      consecutive blocks as bit masks, with two workgroup scans (DPP wave
+//      scans + LDS) per super-tile: block j is chosen if its masked offset is
+//      above T, or equal to T and fewer than need_eq equal ones precede it --
+//      exactly the lowest-index tie rule.
 // With a block table the same pass also takes the set difference (Sec. 2.2:
 // selected blocks whose table entry is -1 are missing) and writes the recall
 // plan: missing blocks in listed order, their count and their run count.
@@ -24,10 +27,72 @@ namespace pulse {
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kKeyCache = 8192;  // middle-block keys kept in LDS (32 KiB); larger requests read L2
+constexpr int kPerThread = kKeyCache / kSelThreads;  // keys (and table entries) prefetched per thread
 
-__device__ inline uint64_t lanemask_lt() {
-    const int lane = threadIdx.x & 63;
-    return lane == 0 ? 0ull : (~0ull >> (64 - lane));
+// Inclusive scan of x over the 64 lanes of a wave with `op`, in registers
+// (DPP row shifts within 16-lane rows, then row broadcasts of lanes 15 and
+// 31); lanes without a source combine with `identity`.
+template <typename Op>
+__device__ inline uint32_t wave_scan(uint32_t x, uint32_t identity, Op op) {
+    const int id = (int)identity;
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x111, 0xF, 0xF, false));  // row_shr:1
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x112, 0xF, 0xF, false));  // row_shr:2
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x114, 0xF, 0xF, false));  // row_shr:4
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x118, 0xF, 0xF, false));  // row_shr:8
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x142, 0xA, 0xF, false));  // row_bcast:15
+    x = op(x, (uint32_t)__builtin_amdgcn_update_dpp(id, (int)x, 0x143, 0xC, 0xF, false));  // row_bcast:31
+    return x;
+}
+struct OpAdd { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a + b; } };
+struct OpMin { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a < b ? a : b; } };
+struct OpMax { __device__ uint32_t operator()(uint32_t a, uint32_t b) const { return a > b ? a : b; } };
+
+// Value of lane 63 (the wave-wide result of an inclusive scan), in every lane.
+__device__ inline uint32_t last_lane(uint32_t x) { return (uint32_t)__builtin_amdgcn_readlane((int)x, 63); }
+
+// Per-wave totals (and each wave's last bit) exchanged through LDS by the
+// workgroup scans of the ordered pass.
+struct ScanLds {
+    uint32_t tot[kSelWaves];
+    uint32_t last[kSelWaves];
+};
+
+// Exclusive prefix sum of v over the workgroup's threads in order; *total =
+// the workgroup sum.  One barrier.
+__device__ inline uint32_t block_scan(uint32_t v, ScanLds& sl, uint32_t& total) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const uint32_t x = wave_scan(v, 0u, OpAdd());  // inclusive scan within the wave
+    if (lane == 63) sl.tot[wid] = x;
+    __syncthreads();
+    uint32_t before = x - v, t = 0;
+#pragma unroll
+    for (int w = 0; w < kSelWaves; ++w) {
+        const uint32_t c = sl.tot[w];
+        if (w < wid) before += c;
+        t += c;
+    }
+    total = t;
+    return before;
+}
+
+// block_scan that also hands each thread the `bit` of the thread before it
+// (thread 0 gets carry_bit) in *prev_bit.
+__device__ inline uint32_t block_scan_last(uint32_t v, uint32_t bit, uint32_t carry_bit, ScanLds& sl,
+                                           uint32_t& total, uint32_t& prev_bit) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    uint32_t pb = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)bit, 0x138, 0xF, 0xF, false);  // wave_shr:1
+    if (lane == 63) sl.last[wid] = bit;
+    const uint32_t before = block_scan(v, sl, total);  // its barrier also publishes sl.last
+    if (lane == 0) pb = wid == 0 ? carry_bit : sl.last[wid - 1];
+    prev_bit = pb;
+    return before;
+}
+
+// Workgroup sum of v (one barrier; sl must not be read concurrently).
+__device__ inline uint32_t block_sum(uint32_t v, ScanLds& sl) {
+    uint32_t total;
+    (void)block_scan(v, sl, total);
+    return total;
 }
 
 // grid = (B, heads): blockIdx.x = request, blockIdx.y = selecting head slot
@@ -42,7 +107,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     __shared__ uint32_t skey[kKeyCache];
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sh_prefix, sh_kk;
-    __shared__ uint32_t wc[kSelWaves][5];
+    __shared__ bool sh_whole;
+    __shared__ uint32_t wc[kSelWaves][2];
+    __shared__ ScanLds scan[2];  // double-buffered: scan[0] equal counts, scan[1] selected / missing
     __shared__ int32_t sh_err;
 
     const int r = blockIdx.x;
@@ -81,68 +148,93 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     }
 
     const bool cached = nc <= kKeyCache;
+    // table entries of this thread's first kPerThread blocks (8*tid ..), loaded
+    // now so their latency overlaps the threshold search
+    const int64_t t_lim = n < max_blocks ? n : max_blocks;  // table entries that exist
+    int32_t tpre[kPerThread];
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+        const int64_t j = (int64_t)kPerThread * tid + u;
+        tpre[u] = -1;
+        if (plan && j < t_lim) tpre[u] = table[(size_t)r * max_blocks + j];
+    }
     const float* msc = scores + b0 + lo;  // middle scores
     const bool all_mid = (k == nc);
     const bool none_mid = (k == 0);
-    uint32_t T = 0, need_eq = 0;
+    // Threshold: a middle block is taken if its masked offset (key - key_base) & T_mask
+    // is above T, or equal to T and fewer than need_eq equal ones precede it.
+    // All keys equal: T_mask = 0, so every key is "equal" and the first k are taken.
+    uint32_t key_base = 0, T = 0, T_mask = 0, need_eq = (uint32_t)k;
     if (!all_mid && !none_mid) {
         // keys to LDS, with the block-wide min and max key
         uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-        for (int64_t i = tid; i < nc; i += kSelThreads) {
-            const uint32_t key = key32(msc[i]);
-            if (cached) skey[i] = key;
-            kmin = min(kmin, key);
-            kmax = max(kmax, key);
-        }
+        if (cached) {  // all loads in flight at once
+            float v[kPerThread];
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, off));
-            kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off));
+            for (int u = 0; u < kPerThread; ++u) {  // nc >= 1 here; clamped, unconditional loads
+                const int64_t i = tid + (int64_t)u * kSelThreads;
+                v[u] = msc[i < nc ? i : nc - 1];
+            }
+#pragma unroll
+            for (int u = 0; u < kPerThread; ++u) {
+                const int64_t i = tid + (int64_t)u * kSelThreads;
+                if (i < nc) {
+                    const uint32_t key = key32(v[u]);
+                    skey[i] = key;
+                    kmin = min(kmin, key);
+                    kmax = max(kmax, key);
+                }
+            }
+        } else {
+            for (int64_t i = tid; i < nc; i += kSelThreads) {
+                const uint32_t key = key32(msc[i]);
+                kmin = min(kmin, key);
+                kmax = max(kmax, key);
+            }
         }
+        kmin = last_lane(wave_scan(kmin, 0xFFFFFFFFu, OpMin()));
+        kmax = last_lane(wave_scan(kmax, 0u, OpMax()));
         if (lane == 0) { wc[wid][0] = kmin; wc[wid][1] = kmax; }
         __syncthreads();
         kmin = 0xFFFFFFFFu;
         kmax = 0u;
         for (int w = 0; w < kSelWaves; ++w) { kmin = min(kmin, wc[w][0]); kmax = max(kmax, wc[w][1]); }
-        __syncthreads();  // wc is reused below
-        const uint32_t diff = kmin ^ kmax;
-        if (diff == 0) {
-            T = kmax;  // every middle key ties: the first k in index order are taken
-            need_eq = (uint32_t)k;
-        } else {
-            // radix passes start at the byte holding the highest bit in which keys differ
-            const int top = 31 - __clz(diff);
-            const int first_shift = (top / 8) * 8;
-            uint32_t mask = first_shift + 8 >= 32 ? 0u : ~((1u << (first_shift + 8)) - 1u);
-            uint32_t prefix = kmax & mask;
+        key_base = kmin;
+        if (kmin != kmax) {
+            // Radix select on the offsets key - kmin (order-preserving, < 2^(top+1)):
+            // digits of 8 bits from bit `top` down, so the first histogram spreads
+            // over the keys' actual range instead of their (shared) exponent byte.
+            // It stops as soon as the bucket holding the k-th offset is taken whole.
+            const uint32_t span = kmax - kmin;
+            const int top = 31 - __clz(span);
+            uint32_t mask = top >= 31 ? 0u : ~((2u << top) - 1u);  // offset bits already decided
+            uint32_t prefix = 0u;                                    // their value
             uint32_t kk = (uint32_t)k;
-            for (int shift = first_shift; shift >= 0; shift -= 8) {
+            for (int shift = top - 7;; shift -= 8) {
+                const int sh = shift > 0 ? shift : 0;
+                const uint32_t dmask = shift >= 0 ? 255u : (255u >> -shift);
                 if (tid < 256) hist[tid] = 0;
                 __syncthreads();
                 for (int64_t i = tid; i < nc; i += kSelThreads) {
-                    const uint32_t key = cached ? skey[i] : key32(msc[i]);
-                    if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+                    const uint32_t off = (cached ? skey[i] : key32(msc[i])) - kmin;
+                    if ((off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
                 }
                 __syncthreads();
                 if (wid == 0) {
                     // lane owns digits 4*lane .. 4*lane+3; find digit d with
-                    // above(d) < kk <= above(d) + hist[d], above(d) = #keys with digit > d.
+                    // above(d) < kk <= above(d) + hist[d], above(d) = #offsets with digit > d.
                     uint32_t c[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) c[i] = hist[4 * lane + i];
                     const uint32_t sum = c[0] + c[1] + c[2] + c[3];
-                    uint32_t x = sum;  // inclusive suffix sum over lanes >= lane
-#pragma unroll
-                    for (int off = 1; off < 64; off <<= 1) {
-                        const uint32_t y = (uint32_t)__shfl_down((int)x, off);
-                        if (lane + off < 64) x += y;
-                    }
-                    uint32_t above = x - sum;
+                    const uint32_t incl = wave_scan(sum, 0u, OpAdd());
+                    uint32_t above = last_lane(incl) - incl;  // offsets in lanes above this one
 #pragma unroll
                     for (int i = 3; i >= 0; --i) {
                         if (above < kk && kk <= above + c[i]) {
-                            sh_prefix = prefix | ((uint32_t)(4 * lane + i) << shift);
+                            sh_prefix = prefix | ((uint32_t)(4 * lane + i) << sh);
                             sh_kk = kk - above;
+                            sh_whole = kk == above + c[i];
                         }
                         above += c[i];
                     }
@@ -150,77 +242,97 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                 __syncthreads();
                 prefix = sh_prefix;
                 kk = sh_kk;
-                mask |= 255u << shift;
+                mask |= dmask << sh;
+                if (sh == 0 || sh_whole) break;
             }
             T = prefix;
+            T_mask = mask;
             need_eq = kk;
         }
     }
 
-    // ordered pass: selection positions, set difference, runs
+    // Ordered pass over super-tiles of kSelThreads * kPerThread blocks; thread t
+    // owns the kPerThread consecutive blocks base + 8t .. base + 8t + 7 as bit
+    // masks.  Two workgroup scans per super-tile: equal-key counts (for the
+    // lowest-index tie rule), then selected / missing counts and each thread's
+    // last missing bit (for run starts).
     uint32_t eq_carry = 0, sel_carry = 0, miss_carry = 0, runs = 0, prev_bit = 0;
     int32_t my_err = 0;
-    for (int64_t tile = 0; tile < n; tile += kSelThreads) {
-        const int64_t j = tile + tid;
-        const bool in = j < n;
-        const bool forced = in && (j < lo || j >= hi);
-        const bool middle = in && !forced;
-        uint32_t key = 0u;
-        if (middle && !all_mid && !none_mid) key = cached ? skey[j - lo] : key32(msc[j - lo]);
-        const bool gt = middle && (all_mid || (!none_mid && key > T));
-        const bool eq = middle && !all_mid && !none_mid && key == T;
-        const uint64_t m_eq = __ballot(eq);
-        if (lane == 0) wc[wid][0] = (uint32_t)__popcll(m_eq);
-        __syncthreads();
-        uint32_t eq_before = eq_carry + (uint32_t)__popcll(m_eq & lanemask_lt()), tile_eq = 0;
-        for (int w = 0; w < kSelWaves; ++w) {
-            if (w < wid) eq_before += wc[w][0];
-            tile_eq += wc[w][0];
-        }
-        const bool sel = forced || gt || (eq && eq_before < need_eq);
-        bool miss = false;
-        if (plan && sel) {
-            if (j >= max_blocks) {
-                my_err = PULSE_ERR_BAD_INDEX;
-            } else {
-                const int32_t v = table[(size_t)r * max_blocks + j];
-                if (v >= n_slots) my_err = PULSE_ERR_BAD_INDEX;
-                else miss = v < 0;
+    const bool thr = !all_mid && !none_mid;
+    for (int64_t base = 0; base < n; base += (int64_t)kSelThreads * kPerThread) {
+        const int64_t j0 = base + (int64_t)kPerThread * tid;
+        uint32_t forced_m = 0, gt_m = 0, eq_m = 0;
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+            const int64_t j = j0 + u;
+            if (j >= n) break;
+            if (j < lo || j >= hi) {
+                forced_m |= 1u << u;
+            } else if (all_mid) {
+                gt_m |= 1u << u;
+            } else if (thr) {
+                const uint32_t key = cached ? skey[j - lo] : key32(msc[j - lo]);
+                const uint32_t mo = (key - key_base) & T_mask;
+                gt_m |= (uint32_t)(mo > T) << u;
+                eq_m |= (uint32_t)(mo == T) << u;
             }
         }
-        const uint64_t m_sel = __ballot(sel);
-        const uint64_t m_miss = __ballot(miss);
-        const uint64_t prev_in_wave = (m_miss << 1);  // bit l = miss flag of lane l-1
-        if (lane == 0) {
-            wc[wid][1] = (uint32_t)__popcll(m_sel);
-            wc[wid][2] = (uint32_t)__popcll(m_miss);
-            wc[wid][3] = (uint32_t)(m_miss >> 63);
+        // scan 1: equal keys before this thread's blocks
+        uint32_t eq_tot;
+        const uint32_t eq_before = eq_carry + block_scan(__popc(eq_m), scan[0], eq_tot);
+        uint32_t take = need_eq > eq_before ? need_eq - eq_before : 0u;  // equal keys still taken
+        uint32_t sel_m = forced_m | gt_m;
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u)
+            if ((eq_m >> u) & 1u) {
+                if (take) { sel_m |= 1u << u; --take; }
+            }
+        // set difference against the block table
+        uint32_t miss_m = 0;
+        if (plan) {
+#pragma unroll
+            for (int u = 0; u < kPerThread; ++u) {
+                if (!((sel_m >> u) & 1u)) continue;
+                const int64_t j = j0 + u;
+                if (j >= t_lim) {
+                    if (j >= max_blocks) my_err = PULSE_ERR_BAD_INDEX;
+                    continue;
+                }
+                const int32_t v = base == 0 ? tpre[u] : table[(size_t)r * max_blocks + j];
+                if (v >= n_slots) my_err = PULSE_ERR_BAD_INDEX;
+                else if (v < 0) miss_m |= 1u << u;
+            }
         }
-        __syncthreads();
-        uint32_t sel_pos = sel_carry + (uint32_t)__popcll(m_sel & lanemask_lt());
-        uint32_t miss_pos = miss_carry + (uint32_t)__popcll(m_miss & lanemask_lt());
-        uint32_t tile_sel = 0, tile_miss = 0;
-        for (int w = 0; w < kSelWaves; ++w) {
-            if (w < wid) { sel_pos += wc[w][1]; miss_pos += wc[w][2]; }
-            tile_sel += wc[w][1];
-            tile_miss += wc[w][2];
+        // scan 2: selected (low 16 bits) and missing (high 16 bits) counts, plus
+        // the previous thread's last missing bit
+        uint32_t tot2;
+        const uint32_t last_bit = (miss_m >> (kPerThread - 1)) & 1u;
+        uint32_t prev_last;
+        const uint32_t before2 =
+            block_scan_last(__popc(sel_m) | ((uint32_t)__popc(miss_m) << 16), last_bit, prev_bit, scan[1], tot2,
+                            prev_last);
+        uint32_t sel_pos = sel_carry + (before2 & 0xFFFFu);
+        uint32_t miss_pos = miss_carry + (before2 >> 16);
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+            const int64_t j = j0 + u;
+            if ((sel_m >> u) & 1u) {
+                if (sel_pos < (uint32_t)k_max) out[sel_pos] = (int32_t)j;
+                ++sel_pos;
+            }
+            if ((miss_m >> u) & 1u) {
+                if (miss_pos < (uint32_t)k_max) miss_list[(size_t)r * k_max + miss_pos] = (int32_t)j;
+                ++miss_pos;
+            }
         }
-        const uint32_t first_prev = wid == 0 ? prev_bit : wc[wid - 1][3];
-        const uint64_t prev_mask = prev_in_wave | (uint64_t)first_prev;
-        const uint64_t starts = m_miss & ~prev_mask;
-        if (sel && sel_pos < (uint32_t)k_max) out[sel_pos] = (int32_t)j;
-        if (miss && miss_pos < (uint32_t)k_max) miss_list[(size_t)r * k_max + miss_pos] = (int32_t)j;
-        if (lane == 0) wc[wid][4] = (uint32_t)__popcll(starts);
-        __syncthreads();
-        uint32_t tile_runs = 0;
-        for (int w = 0; w < kSelWaves; ++w) tile_runs += wc[w][4];
-        runs += tile_runs;
-        prev_bit = wc[kSelWaves - 1][3];
-        eq_carry += tile_eq;
-        sel_carry += tile_sel;
-        miss_carry += tile_miss;
-        __syncthreads();
+        const uint32_t starts = miss_m & ~((miss_m << 1) | prev_last);
+        runs += __popc(starts);
+        prev_bit = scan[1].last[kSelWaves - 1];
+        eq_carry += eq_tot;
+        sel_carry += tot2 & 0xFFFFu;
+        miss_carry += tot2 >> 16;
     }
+    runs = block_sum(runs, scan[0]);
     for (int64_t i = cnt + tid; i < k_max; i += kSelThreads) out[i] = -1;
     if (my_err) atomicCAS(&sh_err, 0, my_err);
     __syncthreads();
