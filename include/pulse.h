@@ -175,6 +175,61 @@ PULSE_API pulse_status pulse_select_headwise(const pulse_shape* shape, const voi
                                              pulse_stream_t stream);
 
 /*
+ * Average selection (Sec. 4.4.1, the "average" strategy SoloHead is compared
+ * with): every KV head h scores the blocks with its own digests
+ * (head_digests[h], laid out as for pulse_select_headwise), the scores are
+ * averaged over the KV heads, in fp32, heads summed in ascending order --
+ * i.e. the mean over all query heads -- and one top-k on the average, with
+ * the sink / local / tie rules of pulse_select_solohead, is shared by all
+ * heads.
+ *   scores   optional device float [total_blocks]: the averaged scores
+ *            (forced blocks are not written); NULL keeps them in ws
+ *   ws       pulse_average_workspace_bytes() bytes of device memory
+ * Other arguments, outputs and errors as for pulse_select_solohead.
+ */
+PULSE_API size_t pulse_average_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t k_max,
+                                               int64_t total_blocks);
+PULSE_API pulse_status pulse_select_average(const pulse_shape* shape, const void* q, const void* head_digests,
+                                            const int64_t* blk_off, int32_t B, int64_t total_blocks,
+                                            const int32_t* k_mid, int32_t n_sink_blocks, int32_t n_local_blocks,
+                                            int32_t k_max, int32_t* sel_idx, int32_t* sel_cnt, float* scores,
+                                            int32_t* dev_status, void* ws, size_t ws_bytes, pulse_stream_t stream);
+
+/*
+ * Middle Attention Mass (Eq. 2, Sec. 4.4.1), the offline calibration that
+ * picks the solo head.  For query head q of request r, MAM_q is the softmax
+ * mass of its full attention over the request's context that falls on the
+ * middle blocks (all blocks except the first n_sink_blocks and the last
+ * n_local_blocks, i.e. the blocks selection ranks); the KV head's MAM is the
+ * mean of MAM_q over its G query heads:
+ *   mam[r][h] = (1/G) sum_g exp(lse_middle(r, hG+g) - lse_all(r, hG+g)),
+ * with lse the natural log-sum-exp of the logits q.k * sm_scale.  Computed
+ * with the sparse attention kernel over every block and over the middle
+ * blocks (fp32; no middle blocks -> 0).
+ *   slot_pool / block_table  as for pulse_sparse_decode_attn; every block of
+ *            every request must be resident (block_table[r][j] valid for
+ *            j < ceil(ctx_len[r] / block_size) <= max_blocks), else
+ *            PULSE_ERR_BAD_INDEX is reported in dev_status
+ *   mam      device float [B][num_kv_heads], written
+ *   ws       pulse_mam_workspace_bytes() bytes of device memory
+ */
+PULSE_API size_t pulse_mam_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t max_blocks);
+PULSE_API pulse_status pulse_mam(const pulse_shape* shape, const void* q, const void* slot_pool, int32_t n_slots,
+                                 const int32_t* block_table, int32_t max_blocks, const int32_t* ctx_len, int32_t B,
+                                 int32_t n_sink_blocks, int32_t n_local_blocks, float sm_scale, float* mam,
+                                 int32_t* dev_status, void* ws, size_t ws_bytes, pulse_stream_t stream);
+
+/*
+ * Solo-head choice from MAM rows (host arrays, [rows][num_kv_heads], e.g. one
+ * row per request or per calibration prompt): the KV head with the highest
+ * summed MAM is the SoloHead (Sec. 4.4.1), the one with the lowest is the
+ * "reversed" choice the paper uses as a control (Sec. 4.4.1, Table of
+ * accuracy results); ties go to the lowest index.  Host-only.
+ */
+PULSE_API pulse_status pulse_pick_solo_heads(const float* mam, int32_t rows, int32_t num_kv_heads, int32_t* solo,
+                                             int32_t* reversed);
+
+/*
  * a4 + a5 + a6. Set difference, slot allocation and gather-scatter recall
  * (Sec. 2.2: B_recall = B_topk minus B_gpu, then copy from DRAM; Sec. 4.4.2:
  * scattered blocks move as coalesced transfers and land in the KV cache).

@@ -213,6 +213,19 @@ def missing_counts(sel_idx, sel_cnt, table):
     return units, runs
 
 
+def average_scores(kv, q, blk_off, ctx_len, Hq, Hkv, bs, d, dtype):
+    """The "average" strategy of Sec. 4.4.1: every KV head scores every block with its
+    own digests (Sec. 4.4.1 with R1, R2), and the fp64 scores are averaged over the KV
+    heads -- the mean over all query heads.  Returns fp64 [total_blocks]; selection on it
+    is select() (R3: the decision is taken on the average rounded once to fp32)."""
+    total = int(blk_off[-1])
+    acc = np.zeros(total, np.float64)
+    for h in range(Hkv):
+        dig = build_digests(kv, blk_off, ctx_len, Hkv, bs, d, dtype, h)
+        acc += score(q, dig, blk_off, Hq, Hkv, d, dtype, h)
+    return acc / Hkv
+
+
 def headwise_select(kv, q, blk_off, ctx_len, Hq, Hkv, bs, d, dtype, k_mid, n_sink, n_local, k_max):
     """Headwise selection baseline (Sec. 3.4; Sec. 4.4.1 'headwise'): every KV head selects
     its own blocks with its own digests.  Returns per-head (sel_idx [Hkv,B,k_max],

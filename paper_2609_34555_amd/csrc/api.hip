@@ -23,7 +23,7 @@ static size_t align_up(size_t x) { return (x + 255) & ~(size_t)255; }
 WsLayout ws_layout(const pulse_shape& s, int32_t B, int32_t k_max, int64_t total_blocks) {
     WsLayout w;
     const size_t G = (size_t)(s.num_q_heads / s.num_kv_heads);
-    const size_t units = (size_t)B * s.num_kv_heads * attn_max_split(k_max, s.block_size);
+    const size_t units = (size_t)attn_partial_units(s, B, k_max);
     size_t o = 0;
     w.scores = o;    o = align_up(o + sizeof(float) * (size_t)total_blocks);
     w.miss_list = o; o = align_up(o + sizeof(int32_t) * (size_t)B * k_max);
@@ -165,6 +165,115 @@ pulse_status pulse_select_headwise(const pulse_shape* shape, const void* q, cons
                       block_table, max_blocks, n_slots, nullptr, miss_list, miss_cnt, run_cnt, req_err, nullptr,
                       dev_status, (int32_t)H, hs);
     return hip_status(e);
+}
+
+size_t pulse_average_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t k_max, int64_t total_blocks) {
+    if (!shape_supported(shape) || B < 0 || k_max < 0 || total_blocks < 0) return 0;
+    const size_t H = (size_t)shape->num_kv_heads;
+    return align_up(sizeof(float) * H * (size_t)total_blocks) + align_up(sizeof(float) * (size_t)total_blocks);
+}
+
+pulse_status pulse_select_average(const pulse_shape* shape, const void* q, const void* head_digests,
+                                  const int64_t* blk_off, int32_t B, int64_t total_blocks, const int32_t* k_mid,
+                                  int32_t n_sink_blocks, int32_t n_local_blocks, int32_t k_max, int32_t* sel_idx,
+                                  int32_t* sel_cnt, float* scores, int32_t* dev_status, void* ws, size_t ws_bytes,
+                                  pulse_stream_t stream) {
+    pulse_status st = check_select_args(shape, q, head_digests, blk_off, B, total_blocks, 0, k_mid, n_sink_blocks,
+                                        n_local_blocks, k_max, sel_idx, sel_cnt, dev_status);
+    if (st != PULSE_OK || B == 0) return st;
+    PULSE_REQUIRE(ws && ws_bytes >= pulse_average_workspace_bytes(shape, B, k_max, total_blocks),
+                  PULSE_ERR_WORKSPACE);
+    const int32_t H = shape->num_kv_heads;
+    float* sc = at<float>(ws, 0);
+    float* avg = scores ? scores : at<float>(ws, align_up(sizeof(float) * (size_t)H * (size_t)total_blocks));
+    hipStream_t hs = (hipStream_t)stream;
+    hipError_t e = launch_score(*shape, q, head_digests, blk_off, B, total_blocks, 0, n_sink_blocks, n_local_blocks,
+                                sc, H, hs);
+    if (e != hipSuccess) return PULSE_ERR_HIP;
+    e = launch_average_scores(sc, total_blocks, H, avg, hs);
+    if (e != hipSuccess) return PULSE_ERR_HIP;
+    e = launch_select(blk_off, B, total_blocks, avg, k_mid, n_sink_blocks, n_local_blocks, k_max, sel_idx, sel_cnt,
+                      nullptr, 0, 0, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, dev_status, 1, hs);
+    return hip_status(e);
+}
+
+// MAM workspace: attention scratch (k_max = max_blocks), then the two
+// selections, their counts, the attention output and the two lse arrays.
+struct MamLayout {
+    WsLayout attn;
+    size_t sel_all, sel_mid, cnt_all, cnt_mid, out, lse_all, lse_mid, total;
+};
+static MamLayout mam_layout(const pulse_shape& s, int32_t B, int32_t max_blocks) {
+    MamLayout m;
+    m.attn = ws_layout(s, B, max_blocks, 0);
+    const size_t sel = sizeof(int32_t) * (size_t)B * max_blocks;
+    size_t o = m.attn.total;
+    m.sel_all = o; o = align_up(o + sel);
+    m.sel_mid = o; o = align_up(o + sel);
+    m.cnt_all = o; o = align_up(o + sizeof(int32_t) * (size_t)B);
+    m.cnt_mid = o; o = align_up(o + sizeof(int32_t) * (size_t)B);
+    m.out = o;     o = align_up(o + sizeof(float) * (size_t)B * s.num_q_heads * kHeadDim);
+    m.lse_all = o; o = align_up(o + sizeof(float) * (size_t)B * s.num_q_heads);
+    m.lse_mid = o; o = align_up(o + sizeof(float) * (size_t)B * s.num_q_heads);
+    m.total = o;
+    return m;
+}
+
+size_t pulse_mam_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t max_blocks) {
+    if (!shape_supported(shape) || B < 0 || max_blocks < 0) return 0;
+    return mam_layout(*shape, B, max_blocks).total;
+}
+
+pulse_status pulse_mam(const pulse_shape* shape, const void* q, const void* slot_pool, int32_t n_slots,
+                       const int32_t* block_table, int32_t max_blocks, const int32_t* ctx_len, int32_t B,
+                       int32_t n_sink_blocks, int32_t n_local_blocks, float sm_scale, float* mam,
+                       int32_t* dev_status, void* ws, size_t ws_bytes, pulse_stream_t stream) {
+    PULSE_REQUIRE(shape, PULSE_ERR_INVALID_ARG);
+    PULSE_REQUIRE(shape_supported(shape), PULSE_ERR_UNSUPPORTED);
+    PULSE_REQUIRE(B >= 0 && max_blocks >= 1 && n_slots >= 1 && n_sink_blocks >= 0 && n_local_blocks >= 0,
+                  PULSE_ERR_INVALID_ARG);
+    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
+    if (B == 0) return PULSE_OK;
+    PULSE_REQUIRE(q && slot_pool && block_table && ctx_len && mam && dev_status, PULSE_ERR_INVALID_ARG);
+    const MamLayout m = mam_layout(*shape, B, max_blocks);
+    PULSE_REQUIRE(ws && ws_bytes >= m.total, PULSE_ERR_WORKSPACE);
+    hipStream_t hs = (hipStream_t)stream;
+    int32_t* sel_all = at<int32_t>(ws, m.sel_all);
+    int32_t* sel_mid = at<int32_t>(ws, m.sel_mid);
+    int32_t* cnt_all = at<int32_t>(ws, m.cnt_all);
+    int32_t* cnt_mid = at<int32_t>(ws, m.cnt_mid);
+    float* out = at<float>(ws, m.out);
+    float* lse_all = at<float>(ws, m.lse_all);
+    float* lse_mid = at<float>(ws, m.lse_mid);
+    hipError_t e = launch_mam_selection(ctx_len, B, shape->block_size, max_blocks, n_sink_blocks, n_local_blocks,
+                                        sel_all, cnt_all, sel_mid, cnt_mid, dev_status, hs);
+    if (e != hipSuccess) return PULSE_ERR_HIP;
+    float* ws_o = at<float>(ws, m.attn.attn_o);
+    float2* ws_ml = at<float2>(ws, m.attn.attn_ml);
+    e = launch_attention(*shape, q, slot_pool, n_slots, block_table, max_blocks, sel_all, cnt_all, max_blocks,
+                         ctx_len, B, sm_scale, out, lse_all, ws_o, ws_ml, dev_status, hs);
+    if (e != hipSuccess) return PULSE_ERR_HIP;
+    e = launch_attention(*shape, q, slot_pool, n_slots, block_table, max_blocks, sel_mid, cnt_mid, max_blocks,
+                         ctx_len, B, sm_scale, out, lse_mid, ws_o, ws_ml, dev_status, hs);
+    if (e != hipSuccess) return PULSE_ERR_HIP;
+    const int32_t G = shape->num_q_heads / shape->num_kv_heads;
+    return hip_status(launch_mam_finalize(lse_all, lse_mid, B, shape->num_kv_heads, G, mam, hs));
+}
+
+pulse_status pulse_pick_solo_heads(const float* mam, int32_t rows, int32_t num_kv_heads, int32_t* solo,
+                                   int32_t* reversed) {
+    PULSE_REQUIRE(mam && rows >= 1 && num_kv_heads >= 1 && solo && reversed, PULSE_ERR_INVALID_ARG);
+    int32_t hi = 0, lo = 0;
+    double vhi = 0.0, vlo = 0.0;
+    for (int32_t h = 0; h < num_kv_heads; ++h) {
+        double s = 0.0;
+        for (int32_t r = 0; r < rows; ++r) s += (double)mam[(size_t)r * num_kv_heads + h];
+        if (h == 0 || s > vhi) { vhi = s; hi = h; }
+        if (h == 0 || s < vlo) { vlo = s; lo = h; }
+    }
+    *solo = hi;
+    *reversed = lo;
+    return PULSE_OK;
 }
 
 static pulse_status check_recall_args(const pulse_shape* shape, const void* host_kv, const int64_t* blk_off,

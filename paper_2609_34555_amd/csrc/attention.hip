@@ -36,10 +36,9 @@ namespace pulse {
 #endif
 constexpr int kCombineThreads = kHeadDim;
 
-// Waves per workgroup: 8 while the LDS merge buffer (waves x G x 128 floats)
-// stays within 32 KiB, else 4.  Fewer, wider workgroups leave fewer partials
-// for the combine kernel.
-inline int attn_waves(int G) { return G <= 8 ? 8 : 4; }
+// Waves per workgroup (attn_waves): 8 while the LDS merge buffer (waves x G x
+// 128 floats) stays within 32 KiB, else 4.  Fewer, wider workgroups leave
+// fewer partials for the combine kernel.
 
 template <int DT>
 struct Mfma;

@@ -68,18 +68,21 @@ struct WsLayout {
     size_t run_cnt;    // int32 [B]
     size_t req_err;    // int32 [B]          per-request plan error (0 = ok)
     size_t misc;       // int32 [16]         [0] = free_head snapshot
-    size_t attn_o;     // float [B][Hkv][max_split][G][d]   (per-workgroup partials)
-    size_t attn_ml;    // float2 [B][Hkv][max_split][G]
+    size_t attn_o;     // float [B][Hkv][n_wg][G][d]   (per-workgroup partials)
+    size_t attn_ml;    // float2 [B][Hkv][n_wg][G]
     size_t total;
 };
 
-// Maximum number of splits any call with these arguments may use.
-inline int32_t attn_max_split(int32_t k_max, int32_t bs) {
-    int64_t chunks = ((int64_t)k_max * bs + kChunkTokens - 1) / kChunkTokens;
-    return (int32_t)(chunks < 1 ? 1 : chunks);
-}
-
 AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs);
+// Waves per attention workgroup for a GQA group of G query heads.
+inline int attn_waves(int G) { return G <= 8 ? 8 : 4; }
+// Attention partials a call with these arguments writes: one per workgroup.
+inline int64_t attn_partial_units(const pulse_shape& s, int32_t B, int32_t k_max) {
+    const int G = s.num_q_heads / s.num_kv_heads;
+    const AttnPlan p = attn_plan(B, s.num_kv_heads, k_max, s.block_size);
+    const int W = attn_waves(G);
+    return (int64_t)B * s.num_kv_heads * ((p.n_split + W - 1) / W);
+}
 WsLayout ws_layout(const pulse_shape& s, int32_t B, int32_t k_max, int64_t total_blocks);
 bool shape_supported(const pulse_shape* s);
 
@@ -122,6 +125,13 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
                             const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t B,
                             float sm_scale, float* out, float* lse, float* ws_o, float2* ws_ml,
                             int32_t* status, hipStream_t st);
+
+hipError_t launch_average_scores(const float* sc, int64_t total_blocks, int32_t H, float* avg, hipStream_t st);
+hipError_t launch_mam_selection(const int32_t* ctx_len, int32_t B, int32_t bs, int32_t max_blocks, int32_t n_sink,
+                                int32_t n_local, int32_t* sel_all, int32_t* cnt_all, int32_t* sel_mid,
+                                int32_t* cnt_mid, int32_t* status, hipStream_t st);
+hipError_t launch_mam_finalize(const float* lse_all, const float* lse_mid, int32_t B, int32_t Hkv, int32_t G,
+                               float* mam, hipStream_t st);
 
 hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 

@@ -183,16 +183,52 @@ class LayerState:
                                    self.sel_cnt, self.k_max, self.ctx_len, w.B, w.sm_scale, self.out, self.lse,
                                    self.dev_status, self.ws, self.ws_bytes, stream=stream)
 
+    def all_head_digests(self, stream=None) -> torch.Tensor:
+        """Digests of every KV head, [Hkv][total_blocks][2][d] (built once)."""
+        w = self.w
+        if getattr(self, "head_digests", None) is None:
+            self.head_digests = torch.zeros((w.Hkv, max(w.total_blocks, 1), 2, w.d), dtype=torch.int16,
+                                            device=self.device)
+            for h in range(w.Hkv):
+                self.build_digests(h, out=self.head_digests[h], stream=stream)
+        return self.head_digests
+
+    def select_average(self, scores: Optional[torch.Tensor] = None, stream=None):
+        """Average selection (all heads' scores averaged) into this step's sel_idx / sel_cnt."""
+        w = self.w
+        hd = self.all_head_digests(stream)
+        nb = P.pulse_average_workspace_bytes(self.shape, w.B, self.k_max, w.total_blocks)
+        ws = torch.zeros(max(nb, 1), dtype=torch.uint8, device=self.device)
+        P.pulse_select_average(self.shape, self.q, hd, self.blk_off, w.B, w.total_blocks, self.k_mid, w.n_sink,
+                               w.n_local, self.k_max, self.sel_idx, self.sel_cnt, scores, self.dev_status, ws, nb,
+                               stream=stream)
+        return ws
+
+    def mam(self, stream=None) -> torch.Tensor:
+        """Middle Attention Mass of every (request, KV head), [B][Hkv], over the whole context:
+        every block is placed in a dense device pool for the calibration."""
+        w = self.w
+        dev = self.device
+        pool = _dev(w.kv, dev)  # slot b = global block b
+        table = np.full((w.B, w.max_blocks), -1, np.int32)
+        for r in range(w.B):
+            n = int(w.n_blocks[r])
+            table[r, :n] = np.arange(int(w.blk_off[r]), int(w.blk_off[r]) + n, dtype=np.int32)
+        table_t = _dev(table, dev)
+        out = torch.zeros((w.B, w.Hkv), dtype=torch.float32, device=dev)
+        nb = P.pulse_mam_workspace_bytes(self.shape, w.B, w.max_blocks)
+        ws = torch.zeros(max(nb, 1), dtype=torch.uint8, device=dev)
+        P.pulse_mam(self.shape, self.q, pool, max(w.total_blocks, 1), table_t, w.max_blocks, self.ctx_len, w.B,
+                    w.n_sink, w.n_local, w.sm_scale, out, self.dev_status, ws, nb, stream=stream)
+        torch.cuda.synchronize()  # the temporary pool, table and workspace are freed on return
+        return out
+
     def headwise(self, stream=None):
         """Headwise selection of every KV head with its own digests against this step's
         table (nothing is recalled).  Returns (sel_idx, sel_cnt, miss_cnt, run_cnt) tensors."""
         w = self.w
         H = w.Hkv
-        if getattr(self, "head_digests", None) is None:
-            self.head_digests = torch.zeros((H, max(w.total_blocks, 1), 2, w.d), dtype=torch.int16,
-                                            device=self.device)
-            for h in range(H):
-                self.build_digests(h, out=self.head_digests[h], stream=stream)
+        self.all_head_digests(stream)
         dev = self.device
         sel_idx = torch.full((H, w.B, self.k_max), -1, dtype=torch.int32, device=dev)
         sel_cnt = torch.zeros((H, w.B), dtype=torch.int32, device=dev)

@@ -33,7 +33,8 @@ EXPORTED = (
     "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms", "pulse_headwise_workspace_bytes",
     "pulse_select_headwise", "pulse_gs_engine_create", "pulse_gs_engine_destroy", "pulse_gs_recall_submit",
     "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing", "pulse_overlap_depth",
-    "pulse_ioaa_plan",
+    "pulse_ioaa_plan", "pulse_average_workspace_bytes", "pulse_select_average", "pulse_mam_workspace_bytes",
+    "pulse_mam", "pulse_pick_solo_heads",
 )
 
 
@@ -110,6 +111,12 @@ def lib():
             "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
             "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
                                                      _P, _P, _P, _P, _P, SZ, _P]),
+            "pulse_average_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+            "pulse_select_average": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, _P, _P, _P, _P,
+                                                    SZ, _P]),
+            "pulse_mam_workspace_bytes": (SZ, [SP, I32, I32]),
+            "pulse_mam": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, I32, I32, I32, F, _P, _P, _P, SZ, _P]),
+            "pulse_pick_solo_heads": (ctypes.c_int, [_P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
             "pulse_gs_engine_create": (ctypes.c_int, [SP, I32, I64, I64, ctypes.POINTER(ctypes.c_void_p)]),
             "pulse_gs_engine_destroy": (ctypes.c_int, [_P]),
             "pulse_gs_recall_submit": (ctypes.c_int, [_P, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
@@ -207,6 +214,44 @@ def pulse_select_headwise(shape, q, head_digests, blk_off, B, total_blocks, k_mi
                                      _ptr(miss_cnt), _ptr(run_cnt), _ptr(dev_status), _ptr(ws), ws_bytes,
                                      _stream(stream))
     return _check(st, "pulse_select_headwise", check)
+
+
+def pulse_average_workspace_bytes(shape: pulse_shape, B: int, k_max: int, total_blocks: int) -> int:
+    return lib().pulse_average_workspace_bytes(ctypes.byref(shape), B, k_max, total_blocks)
+
+
+def pulse_select_average(shape, q, head_digests, blk_off, B, total_blocks, k_mid, n_sink_blocks, n_local_blocks,
+                         k_max, sel_idx, sel_cnt, scores, dev_status, ws, ws_bytes, stream=None, check=True):
+    st = lib().pulse_select_average(ctypes.byref(shape), _ptr(q), _ptr(head_digests), _ptr(blk_off), B,
+                                    total_blocks, _ptr(k_mid), n_sink_blocks, n_local_blocks, k_max, _ptr(sel_idx),
+                                    _ptr(sel_cnt), _ptr(scores), _ptr(dev_status), _ptr(ws), ws_bytes,
+                                    _stream(stream))
+    return _check(st, "pulse_select_average", check)
+
+
+def pulse_mam_workspace_bytes(shape: pulse_shape, B: int, max_blocks: int) -> int:
+    return lib().pulse_mam_workspace_bytes(ctypes.byref(shape), B, max_blocks)
+
+
+def pulse_mam(shape, q, slot_pool, n_slots, block_table, max_blocks, ctx_len, B, n_sink_blocks, n_local_blocks,
+              sm_scale, mam, dev_status, ws, ws_bytes, stream=None, check=True):
+    st = lib().pulse_mam(ctypes.byref(shape), _ptr(q), _ptr(slot_pool), n_slots, _ptr(block_table), max_blocks,
+                         _ptr(ctx_len), B, n_sink_blocks, n_local_blocks, float(sm_scale), _ptr(mam),
+                         _ptr(dev_status), _ptr(ws), ws_bytes, _stream(stream))
+    return _check(st, "pulse_mam", check)
+
+
+def pulse_pick_solo_heads(mam, check=True):
+    """(solo, reversed) KV heads from a host float32 array [rows, num_kv_heads]."""
+    import numpy as np
+
+    m = np.ascontiguousarray(mam, dtype=np.float32)
+    if m.ndim == 1:
+        m = m[None, :]
+    solo, rev = ctypes.c_int32(-1), ctypes.c_int32(-1)
+    st = lib().pulse_pick_solo_heads(_ptr(m), m.shape[0], m.shape[1], ctypes.byref(solo), ctypes.byref(rev))
+    _check(st, "pulse_pick_solo_heads", check)
+    return solo.value, rev.value
 
 
 def pulse_recall_gather(shape, host_kv, blk_off, B, sel_idx, sel_cnt, k_max, block_table, max_blocks, free_slots,

@@ -429,3 +429,64 @@ def test_mam_picks_planted_retrieval_head():
     best, mq, mh = O.mam(w.q, w.kv, w.blk_off, w.ctx_len, 0, w.Hq, w.Hkv, w.bs, w.d, w.dtype_code, w.sm_scale)
     assert best == w.solo_kv_head
     assert mh[best] > 0.999 and np.sort(mh)[-2] < mh[best]
+
+
+# ---------------------------------------------------------------- selection variants (Sec. 4.4.1)
+
+def test_average_bs1_equals_bruteforce_mean_over_all_query_heads():
+    """bs = 1: every head's digest bound is exact, so the averaged score is the exact
+    mean over all Hq query heads of q . k (each query head against its own KV head),
+    and average top-k = brute-force exact top-k of that mean."""
+    w = tiny([120, 77, 9], Hq=8, Hkv=4, d=32, bs=1, seed=41, n_sink=0, n_local=0, k_mid=10)
+    qf = W.to_float(w.q, "bf16").astype(np.float64)
+    K = W.to_float(k_view(w.kv, w.Hkv, 1, w.d)[:, :, 0, :], "bf16").astype(np.float64)
+    avg = O.average_scores(w.kv, w.q, w.blk_off, w.ctx_len, w.Hq, w.Hkv, 1, w.d, O.BF16)
+    rc, idx, cnt = O.select(avg, w.blk_off, np.full(w.B, 10, np.int32), 0, 0, 12)
+    assert rc == 0
+    for r in range(w.B):
+        b0, b1 = int(w.blk_off[r]), int(w.blk_off[r + 1])
+        logit = np.zeros(b1 - b0)
+        for hq in range(w.Hq):
+            logit += K[b0:b1, hq // w.G] @ qf[r, hq]
+        logit /= w.Hq
+        assert np.allclose(avg[b0:b1], logit, rtol=1e-13, atol=1e-12)
+        order = np.lexsort((np.arange(b1 - b0), -logit))
+        assert list(idx[r, : cnt[r]]) == list(np.sort(order[: min(10, b1 - b0)]))
+
+
+def test_average_of_identical_heads_is_the_solohead_score():
+    """All KV heads holding the same keys and every GQA group the same queries: the
+    average over heads equals any single head's SoloHead score."""
+    w = tiny([64, 30], Hq=8, Hkv=4, d=16, bs=4, seed=9)
+    kv = w.kv.reshape(w.total_blocks, 2, w.Hkv, -1).copy()
+    kv[:, :, 1:] = kv[:, :, :1]
+    kv = kv.reshape(w.total_blocks, -1)
+    q = w.q.reshape(w.B, w.Hkv, w.G, w.d).copy()
+    q[:, 1:] = q[:, :1]
+    q = q.reshape(w.B, w.Hq, w.d)
+    avg = O.average_scores(kv, q, w.blk_off, w.ctx_len, w.Hq, w.Hkv, w.bs, w.d, O.BF16)
+    dig = O.build_digests(kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, O.BF16, 2)
+    solo = O.score(q, dig, w.blk_off, w.Hq, w.Hkv, w.d, O.BF16, 2)
+    assert np.allclose(avg, solo, rtol=1e-14, atol=1e-12)
+
+
+def test_mam_over_middle_blocks_equals_bruteforce_softmax_mass():
+    """The block-level middle (all blocks but the first n_sink and last n_local) passed
+    to the token-level Eq. 2 as token counts equals a direct softmax over the raw keys
+    summed over those blocks' tokens (partial last block included)."""
+    w = tiny([45], Hq=4, Hkv=2, d=8, bs=4, seed=17)  # 12 blocks, the last one holds 1 token
+    L, bs, n = int(w.ctx_len[0]), w.bs, int(w.n_blocks[0])
+    ns, nl = 2, 3
+    sink_tok, local_tok = ns * bs, L - (n - nl) * bs
+    best, mq, mh = O.mam(w.q, w.kv, w.blk_off, w.ctx_len, 0, w.Hq, w.Hkv, bs, w.d, O.BF16, w.sm_scale,
+                         sink_tok, local_tok)
+    qf = W.to_float(w.q, "bf16").astype(np.float64)[0]
+    K = W.to_float(k_view(w.kv, w.Hkv, bs, w.d), "bf16").astype(np.float64)  # [blk, h, row, c]
+    for hq in range(w.Hq):
+        keys = K[:, hq // w.G].reshape(-1, w.d)[:L]
+        lg = keys @ qf[hq] * w.sm_scale
+        p = np.exp(lg - lg.max())
+        p /= p.sum()
+        assert abs(mq[hq] - p[ns * bs:(n - nl) * bs].sum()) < 1e-12
+    assert np.allclose(mh, mq.reshape(w.Hkv, w.G).mean(axis=1))
+    assert best == int(np.argmax(mh))

@@ -1,0 +1,151 @@
+"""Selection variants of Sec. 4.4.1 -- Average selection, SoloHead-reversed -- and the
+Middle Attention Mass calibration (Eq. 2) on the GPU, against the oracle."""
+import numpy as np
+import pytest
+
+from oracle import pulse_oracle as O
+from paper_2609_34555_amd import pulse as P
+from paper_2609_34555_amd import workloads as W
+
+MAM_TOL = 1e-4  # absolute, on masses in [0, 1]: fp32 log-sum-exp of the attention kernel
+
+
+# ------------------------------------------------------------------ host side (CPU)
+
+def test_pick_solo_heads_argmax_argmin_lowest_index():
+    rng = np.random.default_rng(0)
+    for _ in range(50):
+        m = rng.integers(0, 4, (3, 8)).astype(np.float32)  # many ties
+        tot = m.astype(np.float64).sum(axis=0)
+        assert P.pulse_pick_solo_heads(m) == (int(np.argmax(tot)), int(np.argmin(tot)))
+    assert P.pulse_pick_solo_heads(np.array([0.2, 0.9, 0.1, 0.9], np.float32)) == (1, 2)
+    with pytest.raises(P.PulseError):
+        P.pulse_pick_solo_heads(np.zeros((0, 4), np.float32))
+
+
+def test_variant_workspace_sizes():
+    sh = P.make_shape(32, 8, 128, 16, W.BF16)
+    assert P.pulse_average_workspace_bytes(sh, 8, 140, 16384) >= 9 * 16384 * 4
+    assert P.pulse_mam_workspace_bytes(sh, 4, 2048) >= 2 * 4 * 2048 * 4 + 4 * 32 * 128 * 4
+    assert P.pulse_mam_workspace_bytes(sh, -1, 10) == 0
+
+
+# ------------------------------------------------------------------ GPU parity
+
+def _oracle_mam(w):
+    """Eq. 2 per request with the block-level middle (first n_sink / last n_local blocks
+    excluded), as token counts for the token-level oracle."""
+    out = np.zeros((w.B, w.Hkv))
+    for r in range(w.B):
+        L, n = int(w.ctx_len[r]), int(w.n_blocks[r])
+        sink_tok = min(w.n_sink * w.bs, L)
+        local_tok = max(0, L - max(n - w.n_local, 0) * w.bs)
+        if n - w.n_sink - w.n_local <= 0:
+            continue  # no middle blocks: MAM 0
+        _, _, mh = O.mam(w.q, w.kv, w.blk_off, w.ctx_len, r, w.Hq, w.Hkv, w.bs, w.d, w.dtype_code, w.sm_scale,
+                         sink_tok, local_tok)
+        out[r] = mh
+    return out
+
+
+AVG_CASES = [
+    ("preset1", dict(cid=1)),
+    ("ragged_g8_bs32", dict(ctx=[3000, 777, 32, 4100], Hq=16, Hkv=2, bs=32, dtype="bf16", k_mid=20)),
+    ("g4_f16_bs16", dict(ctx=[2500, 1, 900], Hq=16, Hkv=4, bs=16, dtype="f16", k_mid=33)),
+]
+
+
+def _workload(kw):
+    if "cid" in kw:
+        return W.preset(kw["cid"])
+    kw = dict(kw)
+    ctx = kw.pop("ctx")
+    return W.custom("v", ctx, planted=True, **kw)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name,kw", AVG_CASES, ids=[c[0] for c in AVG_CASES])
+def test_average_selection_matches_oracle(name, kw):
+    import torch
+    from parity import assert_selection_ok, build, say
+
+    say(f"\n[gpu] average {name}")
+    spec, s = _workload(kw)
+    w, st = build(spec, s)
+    scores = torch.zeros(max(w.total_blocks, 1), dtype=torch.float32, device="cuda")
+    st.select_average(scores=scores)
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    avg = O.average_scores(w.kv, w.q, w.blk_off, w.ctx_len, w.Hq, w.Hkv, w.bs, w.d, w.dtype_code)
+    rc, oidx, ocnt = O.select(avg, w.blk_off, w.k_mid, w.n_sink, w.n_local, st.k_max)
+    assert rc == 0
+    gidx, gcnt = st.selection()
+    n_ties = assert_selection_ok(w, gidx, gcnt, oidx, ocnt, avg)
+    # averaged scores of middle blocks, fp32 accumulation vs exact
+    g = scores.cpu().numpy()
+    for r in range(w.B):
+        b0, n = int(w.blk_off[r]), int(w.n_blocks[r])
+        mid = slice(b0 + w.n_sink, b0 + max(n - w.n_local, w.n_sink))
+        assert np.allclose(g[mid], avg[mid], rtol=2e-5, atol=2e-4 * np.abs(avg).max())
+    say(f"  {w.B} requests, {w.total_blocks} blocks, {n_ties} near-tie differences")
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name,kw", AVG_CASES, ids=[c[0] for c in AVG_CASES])
+def test_mam_and_solohead_choice_match_oracle(name, kw):
+    import torch
+    from parity import assert_selection_ok, build, oracle_selection, say
+
+    say(f"\n[gpu] mam {name}")
+    spec, s = _workload(kw)
+    w, st = build(spec, s)
+    g = st.mam().cpu().numpy()
+    assert st.status() == 0
+    o = _oracle_mam(w)
+    assert np.abs(g - o).max() < MAM_TOL, np.abs(g - o).max()
+    solo, rev = P.pulse_pick_solo_heads(g)
+    tot = o.sum(axis=0)
+    srt = np.sort(tot)
+    if srt[-1] - srt[-2] > 10 * MAM_TOL * w.B:
+        assert solo == int(np.argmax(tot))
+    if srt[1] - srt[0] > 10 * MAM_TOL * w.B:
+        assert rev == int(np.argmin(tot))
+    if kw.get("cid") == 1:
+        assert solo == w.solo_kv_head  # the planted retrieval head
+    # SoloHead-reversed: the same selection path driven by the lowest-MAM head
+    dig = torch.zeros_like(st.digests)
+    st.build_digests(rev, out=dig)
+    torch.cuda.synchronize()
+    P.pulse_select_solohead(st.shape, st.q, dig, st.blk_off, w.B, w.total_blocks, rev, st.k_mid, w.n_sink,
+                             w.n_local, st.k_max, st.sel_idx, st.sel_cnt, None, st.dev_status, st.ws, st.ws_bytes)
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    rc, oidx, ocnt, osc = oracle_selection(w, dig.cpu().numpy().view(np.uint16)[: w.total_blocks], solo=rev)
+    gidx, gcnt = st.selection()
+    assert_selection_ok(w, gidx, gcnt, oidx, ocnt, osc)
+    say(f"  MAM max err {np.abs(g - o).max():.2e}; solo {solo}, reversed {rev}")
+
+
+@pytest.mark.gpu
+def test_mam_reports_missing_block():
+    import torch
+    from parity import build, say
+
+    say("\n[gpu] mam missing block")
+    spec, s = W.custom("v", [300, 100], Hq=8, Hkv=2, bs=16, k_mid=4)
+    w, st = build(spec, s)
+    dev = st.device
+    from paper_2609_34555_amd.harness import _dev
+    pool = _dev(w.kv, dev)
+    table = np.full((w.B, w.max_blocks), -1, np.int32)
+    for r in range(w.B):
+        n = int(w.n_blocks[r])
+        table[r, :n] = np.arange(int(w.blk_off[r]), int(w.blk_off[r]) + n)
+    table[1, 3] = -1  # one block of request 1 not resident
+    out = torch.zeros((w.B, w.Hkv), dtype=torch.float32, device=dev)
+    nb = P.pulse_mam_workspace_bytes(st.shape, w.B, w.max_blocks)
+    ws = torch.zeros(nb, dtype=torch.uint8, device=dev)
+    P.pulse_mam(st.shape, st.q, pool, w.total_blocks, _dev(table, dev), w.max_blocks, st.ctx_len, w.B, w.n_sink,
+                w.n_local, w.sm_scale, out, st.dev_status, ws, nb)
+    torch.cuda.synchronize()
+    assert st.status() == P.PULSE_ERR_BAD_INDEX
