@@ -371,6 +371,107 @@ typedef struct {
  */
 PULSE_API pulse_status pulse_decode_layer(const pulse_layer_args* args, pulse_stream_t stream);
 
+/* ---- Interruptible layer-wise scheduling (IRQ, Sec. 4.2) ---- */
+
+/*
+ * One decode layer of a normal batch (Sec. 4.2: short requests whose KV cache
+ * stays in HBM): decode attention over every block of each request, as
+ * pulse_sparse_decode_attn with every block selected, then a SwiGLU FFN on its
+ * output:
+ *   x = bf16(out) [B][D], D = num_q_heads * head_dim;
+ *   [g | u] = x . w_gate_up^T  [B][2 d_ff];   h = silu(g) * u  [B][d_ff];
+ *   y = h . w_down^T  [B][D]
+ * (bf16 storage, fp32 accumulation; projections and norms are not modelled).
+ * All pointers are device memory owned by the caller:
+ *   w_gate_up bf16 [2 d_ff][D] (gate rows, then up rows); w_down bf16 [D][d_ff];
+ *   x, gu, h, y bf16 scratch / output of the sizes above; out, lse as for
+ *   pulse_sparse_decode_attn; ws pulse_workspace_bytes(shape, B, k_max, 0).
+ */
+typedef struct pulse_normal_layer {
+    pulse_shape shape;
+    int32_t B;
+    const void* q;
+    const void* slot_pool;
+    int32_t n_slots;
+    const int32_t* block_table;
+    int32_t max_blocks;
+    const int32_t* sel_idx;
+    const int32_t* sel_cnt;
+    int32_t k_max;
+    const int32_t* ctx_len;
+    float sm_scale;
+    float* out;
+    float* lse;
+    void* ws;
+    size_t ws_bytes;
+    int32_t d_ff;
+    const void* w_gate_up;
+    const void* w_down;
+    void* x;
+    void* gu;
+    void* h;
+    void* y;
+    int32_t* dev_status;
+} pulse_normal_layer;
+
+/* Completion-detection modes of pulse_irq_step (Sec. 4.2.2). */
+enum {
+    PULSE_IRQ_SEMI_SYNC = 0, /* wait for a normal layer's attention, then check (the paper's choice) */
+    PULSE_IRQ_SYNC = 1,      /* wait for the whole normal layer, then check */
+    PULSE_IRQ_ASYNC = 2,     /* never wait; check between enqueues, at most async_ahead layers queued */
+    PULSE_IRQ_BLOCKING = 3   /* no interleaving: wait for each recall, then one normal layer */
+};
+
+typedef struct pulse_irq_stats {
+    int64_t normal_layers;      /* normal-batch layers run during the step */
+    int32_t offload_layers;     /* offload-batch layers completed */
+    int32_t max_overlap_depth;  /* most normal layers run during one recall */
+    double mean_overlap_depth;  /* normal layers per recall wait (Sec. 4.2.1's overlap depth m) */
+    double wall_ms;             /* host wall time of the step, all work finished */
+    double mean_stall_us;       /* GPU time from a layer's selection to its attention: the offload batch parked */
+    double mean_resume_us;      /* gather kernel path: GPU time from a recall's completion to its attention */
+    double mean_recall_us;      /* gather kernel path: GPU time of a recall (copy + completion signal) */
+} pulse_irq_stats;
+
+typedef struct pulse_irq pulse_irq;
+
+/*
+ * Scheduler state for two caller-owned streams (compute, I/O; default
+ * priority): a pinned host-mapped completion flag, timing events and a
+ * rocBLAS handle bound to the compute stream.  Allocates; not for use inside
+ * stream capture.  Destroy synchronises both streams.
+ */
+PULSE_API pulse_status pulse_irq_create(pulse_stream_t compute_stream, pulse_stream_t io_stream, pulse_irq** irq);
+PULSE_API pulse_status pulse_irq_destroy(pulse_irq* irq);
+
+/*
+ * One decode step of an offload batch -- n_offload_layers chained layer-steps
+ * (pulse_layer_args as for pulse_decode_layer, B >= 1, one per layer) --
+ * interleaved at layer boundaries with a normal batch that cycles through its
+ * n_normal_layers layers (Sec. 4.2.1).  Offload layer m: selection on the
+ * compute stream; recall on the I/O stream, then a signal kernel writes the
+ * layer's sequence number into the pinned flag; until the host sees it, the
+ * host keeps enqueuing normal layers on the compute stream and checks the flag
+ * at each normal layer boundary as `mode` says (ASYNC: at most async_ahead
+ * normal layers queued); then the offload attention for layer m is enqueued
+ * (after a stream wait on the recall) and layer m + 1 follows.  With `engine`
+ * (a pulse_gs_engine for the offload layers' shape) the recall goes through
+ * the gather-scatter engine instead, submitted on the compute stream, and its
+ * host-side completion is the flag; the gather kernel path stalls concurrent
+ * kernels on MI355X while it reads host memory, the engine's DMA does not.
+ * Results of the offload batch are those of pulse_decode_layer on each layer
+ * (mean_resume_us / mean_recall_us are -1 with an engine).
+ * overlap_depth (optional host int32 [n_offload_layers]) receives the normal
+ * layers run during each recall; stats is filled (host).  Returns after both
+ * streams are drained.  A recall whose flag is not seen within 60 s ends the
+ * step with PULSE_ERR_TIMEOUT (after draining); device-side errors are in the
+ * layers' dev_status words.
+ */
+PULSE_API pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int32_t n_offload_layers,
+                                      const pulse_normal_layer* normal, int32_t n_normal_layers, int32_t mode,
+                                      int32_t async_ahead, pulse_gs_engine* engine, int32_t* overlap_depth,
+                                      pulse_irq_stats* stats);
+
 /* ---- IO-Adaptive Offloading Admission (Sec. 4.3; host side) ---- */
 
 typedef struct {

@@ -46,10 +46,6 @@ static T* at(void* ws, size_t off) {
 
 using namespace pulse;
 
-#define PULSE_REQUIRE(cond, code) \
-    do {                          \
-        if (!(cond)) return (code); \
-    } while (0)
 
 static pulse_status hip_status(hipError_t e) { return e == hipSuccess ? PULSE_OK : PULSE_ERR_HIP; }
 
@@ -337,7 +333,46 @@ pulse_status pulse_sparse_decode_attn(const pulse_shape* shape, const void* q, c
                                        at<float2>(ws, w.attn_ml), dev_status, (hipStream_t)stream));
 }
 
-pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream) {
+}  // extern "C"
+
+namespace pulse {
+
+// The three stages of a chained layer-step (arguments already validated).
+// Score + select + recall plan; `mid` (optional) is recorded between score
+// and select.
+hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mid) {
+    const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
+    hipError_t e = launch_score(a.shape, a.q, a.digests, a.blk_off, a.B, a.total_blocks, a.solo_kv_head,
+                                a.n_sink_blocks, a.n_local_blocks, at<float>(a.ws, w.scores), 1, hs);
+    if (e != hipSuccess) return e;
+    if (mid && (e = hipEventRecord(mid, hs)) != hipSuccess) return e;
+    return launch_select(a.blk_off, a.B, a.total_blocks, at<float>(a.ws, w.scores), a.k_mid, a.n_sink_blocks,
+                         a.n_local_blocks, a.k_max, a.sel_idx, a.sel_cnt, a.block_table, a.max_blocks, a.n_slots,
+                         a.free_head, at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt),
+                         at<int32_t>(a.ws, w.run_cnt), at<int32_t>(a.ws, w.req_err), at<int32_t>(a.ws, w.misc),
+                         a.dev_status, 1, hs);
+}
+
+// Gather-scatter recall of the plan written by layer_select.
+hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs) {
+    const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
+    return launch_recall_copy(a.host_kv, a.blk_off, a.B, a.k_max, a.block_table, a.max_blocks, a.free_slots,
+                              a.free_head, a.n_free, a.slot_pool, a.n_slots, pulse_block_bytes(&a.shape),
+                              at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt),
+                              at<int32_t>(a.ws, w.run_cnt), at<int32_t>(a.ws, w.req_err), at<int32_t>(a.ws, w.misc),
+                              a.stats, a.dev_status, hs);
+}
+
+// Sparse attention over the selection.
+hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs) {
+    const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
+    return launch_attention(a.shape, a.q, a.slot_pool, a.n_slots, a.block_table, a.max_blocks, a.sel_idx, a.sel_cnt,
+                            a.k_max, a.ctx_len, a.B, a.sm_scale, a.out, a.lse, at<float>(a.ws, w.attn_o),
+                            at<float2>(a.ws, w.attn_ml), a.dev_status, hs);
+}
+
+// Full argument check of a chained layer-step.
+pulse_status check_layer_args(const pulse_layer_args* a) {
     PULSE_REQUIRE(a, PULSE_ERR_INVALID_ARG);
     pulse_status st = check_select_args(&a->shape, a->q, a->digests, a->blk_off, a->B, a->total_blocks,
                                         a->solo_kv_head, a->k_mid, a->n_sink_blocks, a->n_local_blocks, a->k_max,
@@ -349,35 +384,26 @@ pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream
     if (st != PULSE_OK) return st;
     if (a->B == 0) return PULSE_OK;
     PULSE_REQUIRE(a->ctx_len && a->out, PULSE_ERR_INVALID_ARG);
-    const WsLayout w = ws_layout(a->shape, a->B, a->k_max, a->total_blocks);
-    PULSE_REQUIRE(a->ws && a->ws_bytes >= w.total, PULSE_ERR_WORKSPACE);
+    PULSE_REQUIRE(a->ws && a->ws_bytes >= ws_layout(a->shape, a->B, a->k_max, a->total_blocks).total,
+                  PULSE_ERR_WORKSPACE);
+    return PULSE_OK;
+}
+
+}  // namespace pulse
+
+extern "C" {
+
+pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream) {
+    pulse_status st = check_layer_args(a);
+    if (st != PULSE_OK || a->B == 0) return st;
     hipStream_t hs = (hipStream_t)stream;
-    float* sc = at<float>(a->ws, w.scores);
-    int32_t* miss_list = at<int32_t>(a->ws, w.miss_list);
-    int32_t* miss_cnt = at<int32_t>(a->ws, w.miss_cnt);
-    int32_t* run_cnt = at<int32_t>(a->ws, w.run_cnt);
-    int32_t* req_err = at<int32_t>(a->ws, w.req_err);
-    int32_t* misc = at<int32_t>(a->ws, w.misc);
     hipEvent_t* ev = (hipEvent_t*)a->events;
     if (ev && hipEventRecord(ev[0], hs) != hipSuccess) return PULSE_ERR_HIP;
-    hipError_t e = launch_score(a->shape, a->q, a->digests, a->blk_off, a->B, a->total_blocks, a->solo_kv_head,
-                                a->n_sink_blocks, a->n_local_blocks, sc, 1, hs);
-    if (e != hipSuccess) return PULSE_ERR_HIP;
-    if (ev && hipEventRecord(ev[1], hs) != hipSuccess) return PULSE_ERR_HIP;
-    e = launch_select(a->blk_off, a->B, a->total_blocks, sc, a->k_mid, a->n_sink_blocks, a->n_local_blocks,
-                      a->k_max, a->sel_idx, a->sel_cnt, a->block_table, a->max_blocks, a->n_slots, a->free_head,
-                      miss_list, miss_cnt, run_cnt, req_err, misc, a->dev_status, 1, hs);
-    if (e != hipSuccess) return PULSE_ERR_HIP;
+    if (layer_select(*a, hs, ev ? ev[1] : nullptr) != hipSuccess) return PULSE_ERR_HIP;
     if (ev && hipEventRecord(ev[2], hs) != hipSuccess) return PULSE_ERR_HIP;
-    e = launch_recall_copy(a->host_kv, a->blk_off, a->B, a->k_max, a->block_table, a->max_blocks, a->free_slots,
-                           a->free_head, a->n_free, a->slot_pool, a->n_slots, pulse_block_bytes(&a->shape), miss_list,
-                           miss_cnt, run_cnt, req_err, misc, a->stats, a->dev_status, hs);
-    if (e != hipSuccess) return PULSE_ERR_HIP;
+    if (layer_recall(*a, hs) != hipSuccess) return PULSE_ERR_HIP;
     if (ev && hipEventRecord(ev[3], hs) != hipSuccess) return PULSE_ERR_HIP;
-    e = launch_attention(a->shape, a->q, a->slot_pool, a->n_slots, a->block_table, a->max_blocks, a->sel_idx,
-                         a->sel_cnt, a->k_max, a->ctx_len, a->B, a->sm_scale, a->out, a->lse,
-                         at<float>(a->ws, w.attn_o), at<float2>(a->ws, w.attn_ml), a->dev_status, hs);
-    if (e != hipSuccess) return PULSE_ERR_HIP;
+    if (layer_attention(*a, hs) != hipSuccess) return PULSE_ERR_HIP;
     if (ev && hipEventRecord(ev[4], hs) != hipSuccess) return PULSE_ERR_HIP;
     return PULSE_OK;
 }

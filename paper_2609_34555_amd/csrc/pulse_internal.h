@@ -133,6 +133,25 @@ hipError_t launch_mam_selection(const int32_t* ctx_len, int32_t B, int32_t bs, i
 hipError_t launch_mam_finalize(const float* lse_all, const float* lse_mid, int32_t B, int32_t Hkv, int32_t G,
                                float* mam, hipStream_t st);
 
+// Host-side argument check: return `code` from the calling entry point.
+#define PULSE_REQUIRE(cond, code)   \
+    do {                            \
+        if (!(cond)) return (code); \
+    } while (0)
+
+// Typed pointer at a byte offset of a workspace.
+template <typename T>
+inline T* ws_at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Stages of a chained layer-step (api.hip): score + select + plan, recall,
+// attention; and the full argument check of pulse_layer_args.
+hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mid);
+hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs);
+hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs);
+pulse_status check_layer_args(const pulse_layer_args* a);
+
 hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 
 }  // namespace pulse

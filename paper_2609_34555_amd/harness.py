@@ -9,12 +9,14 @@ beyond the caller-side setup (uploads and state restores).
 from __future__ import annotations
 
 import ctypes
+import math
 from typing import Optional
 
 import numpy as np
 import torch
 
 from . import pulse as P
+from .workloads import BF16 as P_BF16
 from .workloads import Workload
 
 
@@ -316,3 +318,82 @@ class MultiLayerStep:
             st.attention(stream=cmp_)
         cur.wait_stream(io)
         cur.wait_stream(cmp_)
+
+    def run_irq(self, sched, normal=None, mode="semi_sync", async_ahead=4, engine=None):
+        """One step under the interruptible layer-wise scheduler (pulse_irq_step) with an
+        optional NormalBatch and gather-scatter engine; returns (stats dict, per-layer
+        overlap depths)."""
+        torch.cuda.current_stream().synchronize()  # table restores done before the scheduler's streams start
+        args = [st.layer_args() for st in self.layers]
+        return sched.step(args, normal.layers if normal is not None else [], mode=mode, async_ahead=async_ahead,
+                          engine=engine)
+
+
+class NormalBatch:
+    """A normal batch (Sec. 4.2): B requests whose KV cache is resident in HBM, over
+    n_layers layers, each with its own KV pool and SwiGLU FFN weights (seeded random
+    bf16).  ``layers`` holds the pulse_normal_layer structs of the layer scheduler."""
+
+    def __init__(self, B: int, ctx: int, n_layers: int, Hq=32, Hkv=8, d=128, bs=16, d_ff=14336, seed=0,
+                 device="cuda"):
+        dev = torch.device(device)
+        self.B, self.ctx, self.n_layers, self.d_ff = B, ctx, n_layers, d_ff
+        self.shape = P.make_shape(Hq, Hkv, d, bs, P_BF16)
+        n = -(-ctx // bs)
+        self.n_blocks = n
+        E = 2 * Hkv * bs * d
+        D = Hq * d
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        self.table = torch.arange(B * n, dtype=torch.int32, device=dev).reshape(B, n)
+        self.sel_idx = torch.arange(n, dtype=torch.int32, device=dev).repeat(B, 1).contiguous()
+        self.sel_cnt = torch.full((B,), n, dtype=torch.int32, device=dev)
+        self.ctx_len = torch.full((B,), ctx, dtype=torch.int32, device=dev)
+        self.dev_status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.ws_bytes = P.pulse_workspace_bytes(self.shape, B, n, 0)
+        self.bufs = []
+        self.layers = []
+        for _ in range(n_layers):
+            b = {
+                "pool": torch.randn((B * n, E), generator=g, device=dev, dtype=torch.bfloat16).view(torch.int16),
+                "q": torch.randn((B, Hq, d), generator=g, device=dev, dtype=torch.bfloat16),
+                "w_gu": (torch.randn((2 * d_ff, D), generator=g, device=dev, dtype=torch.bfloat16) * 0.02),
+                "w_down": (torch.randn((D, d_ff), generator=g, device=dev, dtype=torch.bfloat16) * 0.02),
+                "out": torch.zeros((B, Hq, d), dtype=torch.float32, device=dev),
+                "lse": torch.zeros((B, Hq), dtype=torch.float32, device=dev),
+                "ws": torch.zeros(max(self.ws_bytes, 1), dtype=torch.uint8, device=dev),
+                "x": torch.zeros((B, D), dtype=torch.bfloat16, device=dev),
+                "gu": torch.zeros((B, 2 * d_ff), dtype=torch.bfloat16, device=dev),
+                "h": torch.zeros((B, d_ff), dtype=torch.bfloat16, device=dev),
+                "y": torch.zeros((B, D), dtype=torch.bfloat16, device=dev),
+            }
+            self.bufs.append(b)
+            L = P.pulse_normal_layer()
+            L.shape = self.shape
+            L.B = B
+            L.q = b["q"].data_ptr()
+            L.slot_pool = b["pool"].data_ptr()
+            L.n_slots = B * n
+            L.block_table = self.table.data_ptr()
+            L.max_blocks = n
+            L.sel_idx = self.sel_idx.data_ptr()
+            L.sel_cnt = self.sel_cnt.data_ptr()
+            L.k_max = n
+            L.ctx_len = self.ctx_len.data_ptr()
+            L.sm_scale = 1.0 / math.sqrt(d)
+            L.out = b["out"].data_ptr()
+            L.lse = b["lse"].data_ptr()
+            L.ws = b["ws"].data_ptr()
+            L.ws_bytes = self.ws_bytes
+            L.d_ff = d_ff
+            L.w_gate_up = b["w_gu"].data_ptr()
+            L.w_down = b["w_down"].data_ptr()
+            L.x = b["x"].data_ptr()
+            L.gu = b["gu"].data_ptr()
+            L.h = b["h"].data_ptr()
+            L.y = b["y"].data_ptr()
+            L.dev_status = self.dev_status.data_ptr()
+            self.layers.append(L)
+
+    def status(self) -> int:
+        return int(self.dev_status.item())

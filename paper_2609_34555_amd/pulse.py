@@ -34,7 +34,7 @@ EXPORTED = (
     "pulse_select_headwise", "pulse_gs_engine_create", "pulse_gs_engine_destroy", "pulse_gs_recall_submit",
     "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing", "pulse_overlap_depth",
     "pulse_ioaa_plan", "pulse_average_workspace_bytes", "pulse_select_average", "pulse_mam_workspace_bytes",
-    "pulse_mam", "pulse_pick_solo_heads",
+    "pulse_mam", "pulse_pick_solo_heads", "pulse_irq_create", "pulse_irq_destroy", "pulse_irq_step",
 )
 
 
@@ -75,6 +75,30 @@ class pulse_layer_args(ctypes.Structure):
         ("dev_status", _P), ("ws", _P), ("ws_bytes", ctypes.c_size_t), ("events", _P),
     ]
 
+
+class pulse_normal_layer(ctypes.Structure):
+    _fields_ = [
+        ("shape", pulse_shape), ("B", ctypes.c_int32), ("q", _P), ("slot_pool", _P), ("n_slots", ctypes.c_int32),
+        ("block_table", _P), ("max_blocks", ctypes.c_int32), ("sel_idx", _P), ("sel_cnt", _P),
+        ("k_max", ctypes.c_int32), ("ctx_len", _P), ("sm_scale", ctypes.c_float), ("out", _P), ("lse", _P),
+        ("ws", _P), ("ws_bytes", ctypes.c_size_t), ("d_ff", ctypes.c_int32), ("w_gate_up", _P), ("w_down", _P),
+        ("x", _P), ("gu", _P), ("h", _P), ("y", _P), ("dev_status", _P),
+    ]
+
+
+class pulse_irq_stats(ctypes.Structure):
+    _fields_ = [("normal_layers", ctypes.c_int64), ("offload_layers", ctypes.c_int32),
+                ("max_overlap_depth", ctypes.c_int32), ("mean_overlap_depth", ctypes.c_double),
+                ("wall_ms", ctypes.c_double), ("mean_stall_us", ctypes.c_double),
+                ("mean_resume_us", ctypes.c_double), ("mean_recall_us", ctypes.c_double)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+PULSE_IRQ_SEMI_SYNC, PULSE_IRQ_SYNC, PULSE_IRQ_ASYNC, PULSE_IRQ_BLOCKING = 0, 1, 2, 3
+IRQ_MODES = {"semi_sync": PULSE_IRQ_SEMI_SYNC, "sync": PULSE_IRQ_SYNC, "async": PULSE_IRQ_ASYNC,
+             "blocking": PULSE_IRQ_BLOCKING}
 
 _lib = None
 
@@ -117,6 +141,11 @@ def lib():
             "pulse_mam_workspace_bytes": (SZ, [SP, I32, I32]),
             "pulse_mam": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, I32, I32, I32, F, _P, _P, _P, SZ, _P]),
             "pulse_pick_solo_heads": (ctypes.c_int, [_P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+            "pulse_irq_create": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_void_p)]),
+            "pulse_irq_destroy": (ctypes.c_int, [_P]),
+            "pulse_irq_step": (ctypes.c_int, [_P, ctypes.POINTER(pulse_layer_args), I32,
+                                              ctypes.POINTER(pulse_normal_layer), I32, I32, I32, _P, _P,
+                                              ctypes.POINTER(pulse_irq_stats)]),
             "pulse_gs_engine_create": (ctypes.c_int, [SP, I32, I64, I64, ctypes.POINTER(ctypes.c_void_p)]),
             "pulse_gs_engine_destroy": (ctypes.c_int, [_P]),
             "pulse_gs_recall_submit": (ctypes.c_int, [_P, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
@@ -252,6 +281,46 @@ def pulse_pick_solo_heads(mam, check=True):
     st = lib().pulse_pick_solo_heads(_ptr(m), m.shape[0], m.shape[1], ctypes.byref(solo), ctypes.byref(rev))
     _check(st, "pulse_pick_solo_heads", check)
     return solo.value, rev.value
+
+
+class IrqScheduler:
+    """pulse_irq_* : interruptible layer-wise scheduling of an offload batch against a
+    normal batch on two streams (compute, I/O)."""
+
+    def __init__(self, compute_stream, io_stream):
+        h = ctypes.c_void_p()
+        _check(lib().pulse_irq_create(_stream(compute_stream), _stream(io_stream), ctypes.byref(h)),
+               "pulse_irq_create", True)
+        self.handle = h
+
+    def step(self, offload_args, normal_layers, mode="semi_sync", async_ahead=4, engine=None, check=True):
+        """offload_args: list of pulse_layer_args; normal_layers: list of pulse_normal_layer;
+        engine: an optional GatherScatterEngine for the recalls.  Returns (stats dict,
+        per-layer overlap depths)."""
+        import numpy as np
+
+        L = len(offload_args)
+        off = (pulse_layer_args * L)(*offload_args)
+        nn = len(normal_layers)
+        nrm = (pulse_normal_layer * max(nn, 1))(*normal_layers) if nn else None
+        depth = np.zeros(L, np.int32)
+        st = pulse_irq_stats()
+        rc = lib().pulse_irq_step(self.handle, off, L, nrm, nn, IRQ_MODES[mode] if isinstance(mode, str) else mode,
+                                  async_ahead, engine.handle if engine is not None else None, depth.ctypes.data,
+                                  ctypes.byref(st))
+        _check(rc, "pulse_irq_step", check)
+        return st.as_dict(), depth
+
+    def destroy(self):
+        if self.handle:
+            lib().pulse_irq_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.destroy()
+        except Exception:
+            pass
 
 
 def pulse_recall_gather(shape, host_kv, blk_off, B, sel_idx, sel_cnt, k_max, block_table, max_blocks, free_slots,

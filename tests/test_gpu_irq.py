@@ -1,0 +1,108 @@
+"""Interruptible layer-wise scheduling (Sec. 4.2) on the GPU: every detection mode must
+leave the offload batch's results identical to the chained single-stream path, and the
+normal batch's layers must compute attention + SwiGLU FFN correctly."""
+import pytest
+import torch
+
+from paper_2609_34555_amd import pulse as P
+from paper_2609_34555_amd.harness import MultiLayerStep, NormalBatch
+
+from parity import say
+
+pytestmark = pytest.mark.gpu
+
+N_OFF, N_NORM = 4, 3
+
+
+@pytest.fixture(scope="module")
+def setup():
+    say("\n[gpu] irq setup")
+    ml = MultiLayerStep(n_layers=N_OFF, n_stores=2, ctx_scale=1 / 8, batch=4)
+    ml.reset()
+    torch.cuda.synchronize()
+    ml.run_chained()
+    torch.cuda.synchronize()
+    ref = [(st.out.clone(), st.lse.clone(), st.table.clone(), st.pool.clone(), st.recall_stats(), st.status())
+           for st in ml.layers]
+    normal = NormalBatch(B=4, ctx=1000, n_layers=N_NORM, d_ff=512, seed=5)
+    sched = P.IrqScheduler(ml.cmp_stream, ml.io_stream)
+    engine = P.GatherScatterEngine(ml.layers[0].shape, 4, max(st.w.B * st.k_max for st in ml.layers), 64)
+    yield ml, ref, normal, sched, engine
+    sched.destroy()
+    engine.destroy()
+
+
+def _ffn_reference(b):
+    """y from the layer's own x, in fp32 with the kernel's bf16 roundings of gu and h."""
+    x = b["x"].float().cpu()
+    wgu = b["w_gu"].float().cpu()
+    wd = b["w_down"].float().cpu()
+    F = wd.shape[1]
+    gu = (x @ wgu.T).bfloat16().float()
+    g, u = gu[:, :F], gu[:, F:]
+    h = (g / (1 + torch.exp(-g)) * u).bfloat16().float()
+    return h @ wd.T
+
+
+@pytest.mark.parametrize("mode,use_engine", [("semi_sync", False), ("sync", False), ("async", False),
+                                             ("blocking", False), ("semi_sync", True), ("blocking", True)])
+def test_irq_mode_matches_chained(setup, mode, use_engine):
+    ml, ref, normal, sched, engine = setup
+    say(f"\n[gpu] irq {mode} engine={use_engine}")
+    ml.reset()
+    normal.dev_status.zero_()
+    torch.cuda.synchronize()
+    stats, depth = ml.run_irq(sched, normal, mode=mode, async_ahead=3,
+                              engine=engine if use_engine else None)
+    torch.cuda.synchronize()
+    say(f"  {stats}  depth {depth.tolist()}")
+    assert stats["offload_layers"] == N_OFF
+    for st, (o, l, t, p, rs, s0) in zip(ml.layers, ref):
+        assert st.status() == s0 == 0
+        assert torch.equal(st.out, o) and torch.equal(st.lse, l)
+        assert torch.equal(st.table, t) and torch.equal(st.pool, p)
+        assert st.recall_stats() == rs
+    assert normal.status() == 0
+    if mode == "blocking":
+        assert stats["normal_layers"] == N_OFF and depth.sum() == 0
+    else:
+        assert depth.sum() == stats["normal_layers"]
+        assert stats["max_overlap_depth"] == depth.max()
+    assert stats["mean_stall_us"] > 0 and stats["wall_ms"] > 0
+    assert (stats["mean_recall_us"] > 0) != use_engine
+
+
+def test_normal_layers_compute_attention_and_ffn(setup):
+    ml, ref, normal, sched, _ = setup
+    say("\n[gpu] irq normal batch numerics")
+    ml.reset()
+    torch.cuda.synchronize()
+    stats, _ = ml.run_irq(sched, normal, mode="blocking")  # one normal layer per offload layer: all 3 run
+    torch.cuda.synchronize()
+    assert stats["normal_layers"] >= N_NORM
+    for li, b in enumerate(normal.bufs):
+        # attention over every resident token, fp32 reference
+        B, Hq, d = b["q"].shape
+        Hkv, bs, n = 8, 16, normal.n_blocks
+        pool = b["pool"].view(torch.bfloat16).float().cpu().reshape(B, n, 2, Hkv, -1)
+        K = pool[:, :, 0].reshape(B, n, Hkv, bs, d).permute(0, 2, 1, 3, 4).reshape(B, Hkv, n * bs, d)
+        V = pool[:, :, 1].reshape(B, n, Hkv, d, bs).permute(0, 2, 1, 4, 3).reshape(B, Hkv, n * bs, d)
+        K, V = K[:, :, : normal.ctx], V[:, :, : normal.ctx]
+        q = b["q"].float().cpu().reshape(B, Hkv, Hq // Hkv, d)
+        s = torch.einsum("bhgd,bhtd->bhgt", q, K) / d ** 0.5
+        want = torch.einsum("bhgt,bhtd->bhgd", torch.softmax(s, -1), V).reshape(B, Hq, d)
+        assert (b["out"].cpu() - want).abs().max() < 2e-3, li
+        assert torch.equal(b["x"].cpu(), b["out"].cpu().reshape(B, -1).bfloat16())
+        y = b["y"].float().cpu()
+        yr = _ffn_reference(b)
+        err = (y - yr).abs().max() / yr.abs().max()
+        say(f"  layer {li}: ffn rel err {err:.2e}")
+        assert err < 2e-2
+
+
+def test_irq_rejects_bad_arguments(setup):
+    ml, ref, normal, sched, _ = setup
+    with pytest.raises(P.PulseError):
+        sched.step([], normal.layers)
+    with pytest.raises(P.PulseError):
+        sched.step([ml.layers[0].layer_args()], normal.layers, mode=7)
