@@ -39,6 +39,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-probes", action="store_true", help="skip link probes and memcpy baselines")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--irq", action="store_true",
+                    help="report: interruptible layer-wise scheduling of a preset-4 offload batch against a "
+                         "resident normal batch, every detection mode and both recall paths (not the default line)")
+    ap.add_argument("--ioaa-profile", action="store_true",
+                    help="report: overlap depth measured over a (B_o, B_n) grid and an IOAA admission on it")
+    ap.add_argument("--normal-batch", type=int, default=32)
     ap.add_argument("--profile", action="store_true",
                     help="profiler run: no CPU baseline or link probes; adds one 256 MiB device copy "
                          "that calibrates the byte counters")
@@ -411,6 +417,104 @@ def bench_multilayer(args, torch, P, H, W):
     return line
 
 
+LLAMA3_8B_FFN = 14336  # d_ff of the Llama-3-8B-shaped layers (d_model 4096 = 32 x 128)
+
+
+def _irq_run(torch, ml, sched, normal, mode, engine, steps):
+    ml.run_irq(sched, normal, mode=mode, engine=engine)  # warm-up
+    rows = []
+    for _ in range(steps):
+        ml.reset()
+        stats, depth = ml.run_irq(sched, normal, mode=mode, engine=engine)
+        for st in ml.layers:
+            if st.status() != 0:
+                raise RuntimeError(f"offload device status {st.status()}")
+        if normal is not None and normal.status() != 0:
+            raise RuntimeError(f"normal device status {normal.status()}")
+        rows.append(stats)
+    return {k: statistics.mean(r[k] for r in rows) for k in rows[0]}
+
+
+def bench_irq(args, torch, P, H):
+    """Interruptible layer-wise scheduling (Sec. 4.2): preset 4's 32-layer offload batch
+    (16 x 64K tokens) against a normal batch of args.normal_batch x 4K-token requests with
+    resident KV and Llama-3-8B-shaped SwiGLU FFNs, 32 layers; every detection mode with the
+    GPU gather kernel and with the gather-scatter engine as the recall path."""
+    ml = H.MultiLayerStep(n_layers=32, n_stores=4)
+    normal = H.NormalBatch(B=args.normal_batch, ctx=4096, n_layers=32, d_ff=LLAMA3_8B_FFN, seed=11)
+    sched = P.IrqScheduler(ml.cmp_stream, ml.io_stream)
+    w0 = ml.layers[0].w
+    engine = P.GatherScatterEngine(ml.layers[0].shape, n_workers=8,
+                                   max_blocks_per_call=max(st.w.B * st.k_max for st in ml.layers),
+                                   staging_blocks=max(1, (16 << 20) // w0.unit_bytes))
+    torch.cuda.synchronize()
+    res = {}
+    try:
+        for path, eng in (("gather_kernel", None), ("gs_engine", engine)):
+            for mode in ("blocking", "semi_sync", "sync", "async"):
+                r = _irq_run(torch, ml, sched, normal, mode, eng, args.steps)
+                wall_s = r["wall_ms"] * 1e-3
+                r["offload_tokens_per_s"] = w0.B / wall_s  # one token per offload request per step
+                r["normal_tokens_per_s"] = normal.B * r["normal_layers"] / normal.n_layers / wall_s
+                res[f"{path}/{mode}"] = r
+                print(f"[irq] {path}/{mode}: wall {r['wall_ms']:.2f} ms, normal layers {r['normal_layers']:.0f}, "
+                      f"depth {r['mean_overlap_depth']:.2f}", file=sys.stderr, flush=True)
+    finally:
+        sched.destroy()
+        engine.destroy()
+    return {"report": "irq", "offload": {"workload": WORKLOADS[4], "layers": 32},
+            "normal": {"batch": normal.B, "ctx": normal.ctx, "layers": normal.n_layers, "d_ff": normal.d_ff,
+                       "d_model": 4096},
+            "steps": args.steps, "results": res}
+
+
+def bench_ioaa(args, torch, P, H):
+    """Overlap depth m(B_o, B_n) measured with IRQ (semi-synchronous, gather-scatter engine)
+    over a grid, then one IOAA admission (Sec. 4.3) of 30 waiting requests on that grid."""
+    import numpy as np
+
+    grid_bo, grid_bn, n_layers = [2, 4, 8, 16], [8, 16, 32], 8
+    m = np.zeros((len(grid_bo), len(grid_bn)))
+    detail = {}
+    for i, bo in enumerate(grid_bo):
+        ml = H.MultiLayerStep(n_layers=n_layers, n_stores=1, batch=bo, ctx_scale=0.5)
+        sched = P.IrqScheduler(ml.cmp_stream, ml.io_stream)
+        engine = P.GatherScatterEngine(ml.layers[0].shape, n_workers=8,
+                                       max_blocks_per_call=max(st.w.B * st.k_max for st in ml.layers),
+                                       staging_blocks=max(1, (16 << 20) // ml.layers[0].w.unit_bytes))
+        try:
+            for j, bn in enumerate(grid_bn):
+                normal = H.NormalBatch(B=bn, ctx=4096, n_layers=n_layers, d_ff=LLAMA3_8B_FFN, seed=13)
+                r = _irq_run(torch, ml, sched, normal, "semi_sync", engine, max(1, args.steps))
+                m[i, j] = max(1.0, r["mean_overlap_depth"])  # one normal layer at least per offload layer
+                detail[f"{bo}x{bn}"] = {"overlap_depth": r["mean_overlap_depth"], "stall_us": r["mean_stall_us"]}
+                print(f"[ioaa] B_o {bo} B_n {bn}: m = {r['mean_overlap_depth']:.2f}", file=sys.stderr, flush=True)
+                del normal
+                torch.cuda.empty_cache()
+        finally:
+            sched.destroy()
+            engine.destroy()
+        del ml
+        torch.cuda.empty_cache()
+    # a waiting queue of 30 requests, lognormal lengths around 16K tokens (sigma 1)
+    rng = np.random.default_rng(2026)
+    lengths = np.clip(rng.lognormal(np.log(16384), 1.0, 30), 1024, 262144).astype(np.int64)
+    kv_per_token = 2 * 8 * 128 * 2 * 32  # K and V, 8 KV heads x 128, bf16, 32 layers
+    digest_bytes = (16384 // 16) * 2 * 128 * 2 * 32  # one head's per-block min/max, 32 layers, 16K tokens
+    params = P.make_ioaa_params(40 << 30, kv_per_token, 2048, digest_bytes, 32, 8, grid_bo, grid_bn, m)
+    t = time.perf_counter()
+    assign, thr, nodes = P.pulse_ioaa_plan(params, lengths)
+    plan_us = (time.perf_counter() - t) * 1e6
+    return {"report": "ioaa", "grid_bo": grid_bo, "grid_bn": grid_bn, "overlap_depth": m.tolist(),
+            "grid_detail": detail, "measured_with": "pulse_irq_step semi_sync + pulse_gs engine, 8 layers, "
+                                                    "offload preset 4 shape at 32K tokens, normal 4K tokens",
+            "queue": {"n": 30, "lengths": lengths.tolist(), "gpu_budget_bytes": 40 << 30,
+                      "running_normal": 32, "running_offload": 8},
+            "plan": {"normal": int((assign == 1).sum()), "offload": int((assign == 2).sum()),
+                     "wait": int((assign == 0).sum()), "throughput_eq1": thr, "nodes_visited": nodes,
+                     "plan_us": plan_us}}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -425,6 +529,10 @@ def main():
     from paper_2609_34555_amd import workloads as W
 
     torch.cuda.set_device(0)
+    if args.irq or args.ioaa_profile:
+        line = bench_irq(args, torch, P, H) if args.irq else bench_ioaa(args, torch, P, H)
+        print(json.dumps(line), flush=True)
+        return
     if args.config == 4:
         line = bench_multilayer(args, torch, P, H, W)
     else:
