@@ -463,9 +463,10 @@ PULSE_API pulse_status pulse_irq_destroy(pulse_irq* irq);
  * (mean_resume_us / mean_recall_us are -1 with an engine).
  * overlap_depth (optional host int32 [n_offload_layers]) receives the normal
  * layers run during each recall; stats is filled (host).  Returns after both
- * streams are drained.  A recall whose flag is not seen within 60 s ends the
- * step with PULSE_ERR_TIMEOUT (after draining); device-side errors are in the
- * layers' dev_status words.
+ * streams (and, after an early exit, an engine call in flight) are drained.
+ * A recall whose flag is not seen within 60 s ends the step with
+ * PULSE_ERR_TIMEOUT (after draining); device-side errors are in the layers'
+ * dev_status words.
  */
 PULSE_API pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int32_t n_offload_layers,
                                       const pulse_normal_layer* normal, int32_t n_normal_layers, int32_t mode,

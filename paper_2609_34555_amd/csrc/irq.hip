@@ -204,6 +204,7 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
     std::vector<hipEvent_t> ring;  // layer-end events of queued normal layers (ASYNC throttle)
     size_t ring_head = 0;
     pulse_status result = PULSE_OK;
+    int64_t engine_pending = 0;  // engine call submitted and not yet seen complete
 
     auto run_normal = [&](bool wait_attn, bool wait_all) -> pulse_status {
         hipEvent_t ea = irq->event(), ee = irq->event();
@@ -243,6 +244,7 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
                                             a.slot_pool, a.n_slots, a.stats, a.dev_status, a.ws, a.ws_bytes, &seq,
                                             irq->cmp);
             if (result != PULSE_OK) break;
+            engine_pending = seq;
         } else {
             seq = ++irq->seq;
             if (hipStreamWaitEvent(irq->io, ev_sel[m], 0) != hipSuccess ||
@@ -260,6 +262,7 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
             if (!engine) return irq->flag_reached(seq);
             int32_t done = 0;
             const pulse_status ps = pulse_gs_recall_poll(engine, seq, &done);
+            if (done) engine_pending = 0;
             if (done && ps != PULSE_OK && result == PULSE_OK) result = ps;
             return done != 0;
         };
@@ -290,8 +293,10 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
             if (result != PULSE_OK) break;
         }
     }
-    // drain both streams (the GPU work enqueued is finite in every case)
+    // drain both streams (the GPU work enqueued is finite in every case) and, after an
+    // early exit, the engine call still in flight, so the engine can take the next one
     const bool ok_sync = hipStreamSynchronize(irq->cmp) == hipSuccess && hipStreamSynchronize(irq->io) == hipSuccess;
+    if (engine && engine_pending) (void)pulse_gs_recall_wait(engine, engine_pending, (int32_t)(wait_limit_s * 1e3));
     if (result == PULSE_OK && !ok_sync) result = PULSE_ERR_HIP;
     const auto t1 = std::chrono::steady_clock::now();
     *stats = pulse_irq_stats{};
