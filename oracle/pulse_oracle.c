@@ -11,7 +11,7 @@
  * Passages followed:
  *   - sparse-offload workflow: select the top-k blocks, take the set
  *     difference against the GPU-resident hot set, copy the missing blocks
- *     from DRAM to the GPU (Sec. 2.2, figure "sparse KV cache offloading");
+ *     from DRAM to the GPU (Sec. 2.2 and its figure of the offloading flow);
  *   - Quest-style per-block key digests and query-digest scores (Sec. 2.1,
  *     Sec. 4.4.1 "average" strategy names the query-digest score);
  *   - SoloHead: one KV head keeps digests and selects a top-k block set that

@@ -20,8 +20,9 @@ blk_off[r] + j.  Tokens past the end of a request's context inside its last
 block are zero.
 
 Planting.  Heavy blocks are planted in the keys of one KV head (the
-retrieval head ``solo_kv_head``).  "The query plus noise" is read as the
-scaled direction of that head's GQA-group mean query: every valid token of a
+retrieval head ``solo_kv_head``).  A heavy block made of the query plus
+0.1 N(0,1) noise is built along the scaled direction of that head's GQA-group
+mean query: every valid token of a
 heavy block gets k = lam * qbar / |qbar|^2 + 0.1 * eps with lam = 2*d, so the
 group-mean logit of a heavy token is lam (before noise).  ``plant_mode =
 "literal"`` instead uses k = q_lead + 0.1 * eps, with q_lead the first query
