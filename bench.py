@@ -258,6 +258,29 @@ def timed_steps(torch, P, st, K, warmup):
     return wall, {k: statistics.mean(v) for k, v in stage.items()}
 
 
+def hbm_probe(torch, P, nbytes, reps=10):
+    """Read bandwidth this GPU sustains over `nbytes` of device memory: the streaming read
+    probe, each launch bracketed by its own HIP events (as the stage events bracket a
+    kernel), mean over `reps` launches after 3 warm-ups.  A spin kernel queued first keeps
+    the GPU busy while the host enqueues the launches, so no host latency is timed."""
+    nbytes = max(16, (int(nbytes) // 16) * 16)
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    sink = torch.zeros(P.pulse_probe_hbm_sink_bytes() // 4, dtype=torch.int32, device="cuda")
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+    for _ in range(3):
+        P.pulse_probe_hbm_read(src, nbytes, sink)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(20_000_000)  # ~10 ms of GPU time ahead of the enqueues below
+    for e0, e1 in evs:
+        e0.record()
+        P.pulse_probe_hbm_read(src, nbytes, sink)
+        e1.record()
+    torch.cuda.synchronize()
+    ms = statistics.mean(e0.elapsed_time(e1) for e0, e1 in evs)
+    del src, sink
+    return nbytes / (ms * 1e-3) / 1e9
+
+
 def rooflines(w, st, mean, rbytes, peak_measured):
     recall_GBps = rbytes / (mean["recall"] * 1e-3) / 1e9
     sel = st.sel_cnt.cpu().numpy()
@@ -312,6 +335,11 @@ def bench_layer(cid, args, torch, P, H, W):
     peak_measured = max([extras["link"]["memcpy_1GiB_GBps"], extras["link"]["kernel_read_1GiB_GBps"]]
                         if "link" in extras else [0.0]) or None
     roof, attn_roof, score_roof = rooflines(w, st, mean, rbytes, peak_measured)
+    if not args.no_probes:  # measured HBM read ceilings at the kernels' own sizes, and at 1 GiB
+        for r in (attn_roof, score_roof):
+            r["peak_measured"] = hbm_probe(torch, P, r["bytes_per_launch"])
+            r["frac_of_measured"] = r["achieved"] / r["peak_measured"]
+        extras["hbm_read_1GiB_GBps"] = hbm_probe(torch, P, 1 << 30)
     if cid == 2:  # the committed counter passes were taken on this workload
         roof["traffic"] = (counter_traffic("recall_copy_kernel") or {}).get("total")
         roof["traffic_split"] = counter_traffic("recall_copy_kernel")

@@ -541,6 +541,16 @@ PULSE_API pulse_status pulse_baseline_memcpy_units(const void* host_kv, void* po
  */
 PULSE_API pulse_status pulse_probe_host_read(const void* host_src, void* dev_dst, size_t bytes, pulse_stream_t stream);
 
+/*
+ * HBM read probe: a streaming kernel that reads `bytes` (a multiple of 16) of
+ * device memory at `src` and folds them into one word per workgroup in
+ * `sink` (device, pulse_probe_hbm_sink_bytes() bytes).  Timed over the byte
+ * count of an HBM-bound kernel, it measures the read bandwidth the GPU
+ * sustains at that size.
+ */
+PULSE_API pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, pulse_stream_t stream);
+PULSE_API size_t pulse_probe_hbm_sink_bytes(void);
+
 /* Timing events for pulse_layer_args.events: n hipEvent_t handles written to
  * events[0..n); destroy with pulse_events_destroy. */
 PULSE_API pulse_status pulse_events_create(int32_t n, void** events);

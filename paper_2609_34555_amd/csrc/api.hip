@@ -408,6 +408,13 @@ pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream
     return PULSE_OK;
 }
 
+pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, pulse_stream_t stream) {
+    PULSE_REQUIRE(bytes % 16 == 0 && (src || bytes == 0) && sink, PULSE_ERR_INVALID_ARG);
+    return hip_status(launch_probe_hbm_read(src, bytes, (uint32_t*)sink, (hipStream_t)stream));
+}
+
+size_t pulse_probe_hbm_sink_bytes(void) { return sizeof(uint32_t) * (size_t)probe_hbm_sink_words(); }
+
 pulse_status pulse_events_create(int32_t n, void** events) {
     PULSE_REQUIRE(n >= 0 && (events || n == 0), PULSE_ERR_INVALID_ARG);
     for (int32_t i = 0; i < n; ++i) {

@@ -152,6 +152,9 @@ hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs);
 hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs);
 pulse_status check_layer_args(const pulse_layer_args* a);
 
+hipError_t launch_probe_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st);
+int32_t probe_hbm_sink_words();
+
 hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 
 }  // namespace pulse

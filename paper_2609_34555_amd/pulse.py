@@ -35,6 +35,7 @@ EXPORTED = (
     "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing", "pulse_overlap_depth",
     "pulse_ioaa_plan", "pulse_average_workspace_bytes", "pulse_select_average", "pulse_mam_workspace_bytes",
     "pulse_mam", "pulse_pick_solo_heads", "pulse_irq_create", "pulse_irq_destroy", "pulse_irq_step",
+    "pulse_probe_hbm_read", "pulse_probe_hbm_sink_bytes",
 )
 
 
@@ -132,6 +133,8 @@ def lib():
             "pulse_host_free": (ctypes.c_int, [_P]),
             "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
             "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
+            "pulse_probe_hbm_read": (ctypes.c_int, [_P, SZ, _P, _P]),
+            "pulse_probe_hbm_sink_bytes": (SZ, []),
             "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
             "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
                                                      _P, _P, _P, _P, _P, SZ, _P]),
@@ -366,6 +369,15 @@ def pulse_baseline_memcpy_units(host_kv, pool, src_units, dst_units, n, unit_byt
 def pulse_probe_host_read(host_src, dev_dst, nbytes, stream=None, check=True):
     st = lib().pulse_probe_host_read(_ptr(host_src), _ptr(dev_dst), nbytes, _stream(stream))
     return _check(st, "pulse_probe_host_read", check)
+
+
+def pulse_probe_hbm_read(src, nbytes, sink, stream=None, check=True):
+    st = lib().pulse_probe_hbm_read(_ptr(src), nbytes, _ptr(sink), _stream(stream))
+    return _check(st, "pulse_probe_hbm_read", check)
+
+
+def pulse_probe_hbm_sink_bytes() -> int:
+    return lib().pulse_probe_hbm_sink_bytes()
 
 
 def make_ioaa_params(gpu_budget_bytes, kv_bytes_per_token, offload_tokens, offload_extra_bytes, running_normal,
