@@ -13,7 +13,7 @@
  *     difference against the GPU-resident hot set, copy the missing blocks
  *     from DRAM to the GPU (Sec. 2.2 and its figure of the offloading flow);
  *   - Quest-style per-block key digests and query-digest scores (Sec. 2.1,
- *     Sec. 4.4.1 "average" strategy names the query-digest score);
+ *     Sec. 4.4.1, where the averaged strategy speaks of query-digest scores);
  *   - SoloHead: one KV head keeps digests and selects a top-k block set that
  *     every KV head of the layer shares (Sec. 4.4.1);
  *   - hot set = sink + local + selected middle tokens; sink and local stay
@@ -23,25 +23,34 @@
  *   - gather the scattered blocks, one large copy, scatter into the GPU KV
  *     cache (Sec. 4.4.2).
  *
- * Readings taken where the paper is silent (each is restated in the design
- * notes of the repository):
+ * Readings taken where the paper is silent (numbered as in the repository's
+ * list of readings; R10-R12 concern inputs and tests, not this arithmetic):
  *   R1  digest = per-block, per-channel min and max of the keys over the
  *       block's valid tokens, kept in the KV dtype; -0 orders below +0.
  *   R2  score = (1/G) * sum_g sum_c max(q_gc*mn_c, q_gc*mx_c) over the G
  *       query heads of the solo KV head (mean of per-query-head bounds);
  *       no 1/sqrt(d) factor (it does not change the ranking).
  *   R3  the selection decision is taken on the exact score rounded once to
- *       fp32; equal fp32 keys are ordered by ascending block index.
- *   R4  forced blocks: the first n_sink and the last n_local blocks of a
- *       request; k' = min(max(k_mid,0), #middle) middle blocks are chosen;
- *       the selection is emitted in ascending block order.
- *   R5  missing blocks are taken in (request asc, listed order) order; the
- *       i-th gets free_slots[free_head + i]; a run is a maximal stretch of
- *       listed missing blocks whose indices increase by exactly one.
- *   R6  attention: softmax over the valid tokens of the selected blocks of
+ *       fp32.
+ *   R4  equal fp32 keys are ordered by ascending block index; the selection
+ *       is emitted in ascending block order.
+ *   R5  forced blocks: the first n_sink and the last n_local blocks of a
+ *       request; k' = min(max(k_mid,0), #middle) middle blocks are chosen.
+ *   R6  missing blocks are taken in (request asc, listed order) order; the
+ *       i-th gets free_slots[free_head + i].
+ *   R7  a run is a maximal stretch of listed missing blocks of one request
+ *       whose indices increase by exactly one.
+ *   R8  digests and attention use the valid tokens of a partial last block
+ *       only.
+ *   R9  attention: softmax over the valid tokens of the selected blocks of
  *       sm_scale * q.k, output sum_t p_t v_t, lse = log sum_t exp(logit_t);
- *       an empty selection gives out = 0, lse = -inf.
- *   R7  KV head of query head hq is hq / G (consecutive GQA groups).
+ *       an empty selection gives out = 0, lse = -inf; the KV head of query
+ *       head hq is hq / G (consecutive GQA groups).
+ *   R13 MAM's middle tokens are those outside the sink and local token
+ *       counts the caller passes (block-aligned counts give the blocks that
+ *       selection ranks).
+ *   R14 (pulse_oracle.py) the Average strategy averages the per-KV-head
+ *       scores of R2 over the KV heads: the mean over all query heads.
  *
  * Block layout, in 16-bit elements, of one KV block of Hkv heads (host store
  * and slot pool alike):
@@ -177,7 +186,7 @@ int or_score(const uint16_t* q, const uint16_t* digests, const int64_t* blk_off,
     return OR_OK;
 }
 
-/* ---- a3: SoloHead top-k block selection (Sec. 4.4.1, Sec. 5 setup; R3, R4) */
+/* ---- a3: SoloHead top-k block selection (Sec. 4.4.1, Sec. 5 setup; R3-R5) */
 
 typedef struct {
     float key;
@@ -235,7 +244,7 @@ int or_select(const double* scores, const int64_t* blk_off, int B, const int32_t
 }
 
 /* ---- a4-a6: set difference, slot allocation, gather-scatter recall
- *      (Sec. 2.2, Sec. 4.4.2; R5) ------------------------------------------ */
+ *      (Sec. 2.2, Sec. 4.4.2; R6, R7) -------------------------------------- */
 
 int or_recall(const uint8_t* host_kv, const int64_t* blk_off, int B, const int32_t* sel_idx,
               const int32_t* sel_cnt, int k_max, int32_t* table, int max_blocks,
@@ -289,7 +298,7 @@ int or_recall(const uint8_t* host_kv, const int64_t* blk_off, int B, const int32
 }
 
 /* ---- a7: sparse GQA decode attention over the selected blocks
- *      (Sec. 2.2 attention after recall, Sec. 4.2.1; R6, R7) --------------- */
+ *      (Sec. 2.2 attention after recall, Sec. 4.2.1; R8, R9) --------------- */
 
 static void attend_one(const uint16_t* qrow, const uint16_t* const* blocks, const int* nvalid,
                        int nb, int Hkv, int bs, int d, int dtype, int h, double sm_scale,

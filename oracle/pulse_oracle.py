@@ -183,7 +183,9 @@ def dense_attention(q, host_kv, blk_off, ctx_len, Hq, Hkv, bs, d, dtype, sm_scal
 
 def mam(q, host_kv, blk_off, ctx_len, r, Hq, Hkv, bs, d, dtype, sm_scale, n_sink_tok=16,
         n_local_tok=128):
-    """Middle Attention Mass, Eq. 2, of request r; returns (best_kv_head, mam_q, mam_h)."""
+    """Middle Attention Mass, Eq. 2, of request r; returns (best_kv_head, mam_q, mam_h).
+    The middle excludes the first n_sink_tok and last n_local_tok tokens (R13: the tests
+    pass the token counts of the sink and local blocks)."""
     q = _c(q, np.uint16)
     host_kv = _c(host_kv, np.uint16)
     blk_off = _c(blk_off, np.int64)
@@ -215,7 +217,7 @@ def missing_counts(sel_idx, sel_cnt, table):
 
 def average_scores(kv, q, blk_off, ctx_len, Hq, Hkv, bs, d, dtype):
     """The "average" strategy of Sec. 4.4.1: every KV head scores every block with its
-    own digests (Sec. 4.4.1 with R1, R2), and the fp64 scores are averaged over the KV
+    own digests (Sec. 4.4.1 with R1, R2), and (R14) the fp64 scores are averaged over the KV
     heads -- the mean over all query heads.  Returns fp64 [total_blocks]; selection on it
     is select() (R3: the decision is taken on the average rounded once to fp32)."""
     total = int(blk_off[-1])
