@@ -175,6 +175,27 @@ PULSE_API pulse_status pulse_select_headwise(const pulse_shape* shape, const voi
                                              pulse_stream_t stream);
 
 /*
+ * Step-end release of a recall: the hot set is fixed-size (Sec. 4.2: sink,
+ * local and hot middle blocks stay resident; recalled blocks serve one layer
+ * step), so after the step's attention the blocks the last recall mapped go
+ * back to "not resident" (block_table entry -1) and their slots back to the
+ * free list: *free_head -= stats.n_missing, then stats is cleared.  This is
+ * the exact undo of that recall (allocation is LIFO from the free list), so
+ * no allocation may happen between the recall and its release.  Reads the
+ * recall plan (missing blocks per request) that the recall left in `ws`:
+ * pass the workspace, B, k_max and total_blocks of the call that planned it
+ * (pulse_decode_layer: its total_blocks; pulse_recall_gather and the
+ * gather-scatter engine: 0).  A recall that moved no bytes (exhaustion, an
+ * error, nothing missing) is not undone; a second release is a no-op.
+ * Stream-ordered, no host sync; inconsistent plans report BAD_INDEX in
+ * dev_status.
+ */
+PULSE_API pulse_status pulse_release_recalled(const pulse_shape* shape, int32_t B, int32_t k_max,
+                                              int64_t total_blocks, int32_t* block_table, int32_t max_blocks,
+                                              int32_t* free_head, pulse_recall_stats* stats, int32_t* dev_status,
+                                              void* ws, size_t ws_bytes, pulse_stream_t stream);
+
+/*
  * Average selection (Sec. 4.4.1, the "average" strategy SoloHead is compared
  * with): every KV head h scores the blocks with its own digests
  * (head_digests[h], laid out as for pulse_select_headwise), the scores are

@@ -315,6 +315,22 @@ pulse_status pulse_recall_gather(const pulse_shape* shape, const void* host_kv, 
     return hip_status(e);
 }
 
+pulse_status pulse_release_recalled(const pulse_shape* shape, int32_t B, int32_t k_max, int64_t total_blocks,
+                                    int32_t* block_table, int32_t max_blocks, int32_t* free_head,
+                                    pulse_recall_stats* stats, int32_t* dev_status, void* ws, size_t ws_bytes,
+                                    pulse_stream_t stream) {
+    PULSE_REQUIRE(shape, PULSE_ERR_INVALID_ARG);
+    PULSE_REQUIRE(shape_supported(shape), PULSE_ERR_UNSUPPORTED);
+    PULSE_REQUIRE(B >= 0 && k_max >= 1 && max_blocks >= 1 && total_blocks >= 0, PULSE_ERR_INVALID_ARG);
+    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
+    if (B == 0) return PULSE_OK;
+    PULSE_REQUIRE(block_table && free_head && stats && dev_status, PULSE_ERR_INVALID_ARG);
+    const WsLayout w = ws_layout(*shape, B, k_max, total_blocks);
+    PULSE_REQUIRE(ws && ws_bytes >= w.total, PULSE_ERR_WORKSPACE);
+    return hip_status(launch_release(at<int32_t>(ws, w.miss_list), at<int32_t>(ws, w.miss_cnt), B, k_max, block_table,
+                                     max_blocks, free_head, stats, dev_status, (hipStream_t)stream));
+}
+
 pulse_status pulse_sparse_decode_attn(const pulse_shape* shape, const void* q, const void* slot_pool, int32_t n_slots,
                                       const int32_t* block_table, int32_t max_blocks, const int32_t* sel_idx,
                                       const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t B,

@@ -152,6 +152,9 @@ hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs);
 hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs);
 pulse_status check_layer_args(const pulse_layer_args* a);
 
+hipError_t launch_release(const int32_t* miss_list, const int32_t* miss_cnt, int32_t B, int32_t k_max,
+                          int32_t* table, int32_t max_blocks, int32_t* free_head, pulse_recall_stats* stats,
+                          int32_t* status, hipStream_t st);
 hipError_t launch_probe_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st);
 int32_t probe_hbm_sink_words();
 

@@ -188,6 +188,52 @@ __global__ __launch_bounds__(kCopyThreads) void probe_copy_kernel(const uint8_t*
         copy_chunk<4>(src + c * 16384, dst + c * 16384, threadIdx.x);
 }
 
+// Step-end release of a recall (undo, LIFO): every block the last recall
+// mapped returns to "not resident" and its slot to the free list.  Phase 1
+// (grid B): clear the table entries of the plan's missing blocks when the
+// recall moved bytes; phase 2 (one thread): give the slots back and clear the
+// statistics, so a second release changes nothing.
+__global__ __launch_bounds__(kCopyThreads) void release_table_kernel(
+    const int32_t* __restrict__ miss_list, const int32_t* __restrict__ miss_cnt, int32_t k_max,
+    int32_t* __restrict__ table, int32_t max_blocks, const pulse_recall_stats* __restrict__ stats, int32_t* status) {
+    if (stats->bytes <= 0) return;
+    const int r = blockIdx.x;
+    int32_t n = miss_cnt[r];
+    if (n < 0 || n > k_max) {
+        if (threadIdx.x == 0) report(status, PULSE_ERR_BAD_INDEX);
+        return;
+    }
+    for (int i = threadIdx.x; i < n; i += kCopyThreads) {
+        const int32_t j = miss_list[(size_t)r * k_max + i];
+        if (j >= 0 && j < max_blocks) table[(size_t)r * max_blocks + j] = -1;
+        else report(status, PULSE_ERR_BAD_INDEX);
+    }
+}
+
+__global__ void release_head_kernel(int32_t* free_head, pulse_recall_stats* stats, int32_t* status) {
+    if (threadIdx.x != 0 || blockIdx.x != 0 || stats->bytes <= 0) return;
+    if (*free_head < stats->n_missing) {
+        report(status, PULSE_ERR_BAD_INDEX);
+        return;
+    }
+    *free_head -= stats->n_missing;
+    stats->n_missing = 0;
+    stats->n_runs = 0;
+    stats->bytes = 0;
+}
+
+hipError_t launch_release(const int32_t* miss_list, const int32_t* miss_cnt, int32_t B, int32_t k_max,
+                          int32_t* table, int32_t max_blocks, int32_t* free_head, pulse_recall_stats* stats,
+                          int32_t* status, hipStream_t st) {
+    if (B == 0) return hipSuccess;
+    hipLaunchKernelGGL(release_table_kernel, dim3((unsigned)B), dim3(kCopyThreads), 0, st, miss_list, miss_cnt, k_max,
+                       table, max_blocks, stats, status);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(release_head_kernel, dim3(1), dim3(64), 0, st, free_head, stats, status);
+    return hipGetLastError();
+}
+
 hipError_t launch_recall_plan(const int64_t* blk_off, int32_t B, const int32_t* sel_idx, const int32_t* sel_cnt,
                               int32_t k_max, const int32_t* table, int32_t max_blocks, int32_t n_slots,
                               const int32_t* free_head, int32_t* miss_list, int32_t* miss_cnt, int32_t* run_cnt,

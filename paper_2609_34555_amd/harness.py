@@ -156,6 +156,15 @@ class LayerState:
     def decode_layer(self, stream=None):
         P.pulse_decode_layer(self.layer_args(), stream=stream)
 
+    def release(self, chained=True, stream=None):
+        """Step-end release of the last recall (pulse_release_recalled): table and free
+        head return to their state before it.  chained: the recall came from
+        decode_layer (else from recall() / the engine)."""
+        w = self.w
+        P.pulse_release_recalled(self.shape, w.B, self.k_max, w.total_blocks if chained else 0, self.table,
+                                 w.max_blocks, self.free_head, self.stats, self.dev_status, self.ws, self.ws_bytes,
+                                 stream=stream)
+
     def select(self, scores: Optional[torch.Tensor] = None, stream=None):
         w = self.w
         P.pulse_select_solohead(self.shape, self.q, self.digests, self.blk_off, w.B, w.total_blocks, w.solo_kv_head,

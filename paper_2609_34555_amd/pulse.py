@@ -35,7 +35,7 @@ EXPORTED = (
     "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing", "pulse_overlap_depth",
     "pulse_ioaa_plan", "pulse_average_workspace_bytes", "pulse_select_average", "pulse_mam_workspace_bytes",
     "pulse_mam", "pulse_pick_solo_heads", "pulse_irq_create", "pulse_irq_destroy", "pulse_irq_step",
-    "pulse_probe_hbm_read", "pulse_probe_hbm_sink_bytes",
+    "pulse_probe_hbm_read", "pulse_probe_hbm_sink_bytes", "pulse_release_recalled",
 )
 
 
@@ -134,6 +134,7 @@ def lib():
             "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
             "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
             "pulse_probe_hbm_read": (ctypes.c_int, [_P, SZ, _P, _P]),
+            "pulse_release_recalled": (ctypes.c_int, [SP, I32, I32, I64, _P, I32, _P, _P, _P, _P, SZ, _P]),
             "pulse_probe_hbm_sink_bytes": (SZ, []),
             "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
             "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
@@ -334,6 +335,14 @@ def pulse_recall_gather(shape, host_kv, blk_off, B, sel_idx, sel_cnt, k_max, blo
                                    _ptr(free_head), n_free, _ptr(slot_pool), n_slots, _ptr(stats), _ptr(dev_status),
                                    _ptr(ws), ws_bytes, _stream(stream))
     return _check(st, "pulse_recall_gather", check)
+
+
+def pulse_release_recalled(shape, B, k_max, total_blocks, block_table, max_blocks, free_head, stats, dev_status,
+                           ws, ws_bytes, stream=None, check=True):
+    st = lib().pulse_release_recalled(ctypes.byref(shape), B, k_max, total_blocks, _ptr(block_table), max_blocks,
+                                      _ptr(free_head), _ptr(stats), _ptr(dev_status), _ptr(ws), ws_bytes,
+                                      _stream(stream))
+    return _check(st, "pulse_release_recalled", check)
 
 
 def pulse_sparse_decode_attn(shape, q, slot_pool, n_slots, block_table, max_blocks, sel_idx, sel_cnt, k_max,
