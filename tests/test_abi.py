@@ -109,6 +109,30 @@ def test_probe_and_baseline_validation():
         P.PULSE_ERR_INVALID_ARG
 
 
+def test_new_entry_points_validation_codes():
+    sh = shape()
+    # B above the supported maximum
+    assert P.pulse_release_recalled(sh, 4097, 16, 10, FAKE, 100, FAKE, FAKE, FAKE, FAKE, 1 << 30, stream=0,
+                                    check=False) == P.PULSE_ERR_UNSUPPORTED
+    assert P.pulse_release_recalled(sh, 2, 16, 10, FAKE, 100, FAKE, FAKE, FAKE, FAKE, 1, stream=0,
+                                    check=False) == P.PULSE_ERR_WORKSPACE
+    assert P.pulse_release_recalled(sh, 0, 16, 10, None, 100, None, None, None, None, 0, stream=0,
+                                    check=False) == P.PULSE_OK
+    assert P.pulse_select_average(sh, FAKE, FAKE, FAKE, 2, 10, FAKE, 1, 8, 16, FAKE, FAKE, None, FAKE, FAKE, 1,
+                                  stream=0, check=False) == P.PULSE_ERR_WORKSPACE
+    assert P.pulse_mam(sh, FAKE, FAKE, 10, FAKE, 0, FAKE, 2, 1, 8, 0.1, FAKE, FAKE, FAKE, 1 << 30, stream=0,
+                       check=False) == P.PULSE_ERR_INVALID_ARG
+    assert P.pulse_mam(sh, FAKE, FAKE, 10, FAKE, 100, FAKE, 2, 1, 8, 0.1, FAKE, FAKE, FAKE, 1, stream=0,
+                       check=False) == P.PULSE_ERR_WORKSPACE
+    assert P.pulse_probe_hbm_read(FAKE, 1000, FAKE, stream=0, check=False) == P.PULSE_ERR_INVALID_ARG
+    assert P.lib().pulse_irq_step(None, None, 1, None, 0, 0, 1, None, None, None) == P.PULSE_ERR_INVALID_ARG
+    la = P.pulse_layer_args()
+    la.shape = sh
+    la.B = 4097
+    la.k_max, la.max_blocks, la.n_free, la.n_slots, la.n_sink_blocks, la.n_local_blocks = 16, 100, 10, 50, 1, 8
+    assert P.pulse_decode_layer(la, stream=0, check=False) == P.PULSE_ERR_UNSUPPORTED
+
+
 def test_oracle_and_product_share_nothing():
     """The oracle never imports the GPU package and the GPU package never imports the oracle."""
     pkg = os.path.join(ROOT, "paper_2609_34555_amd")

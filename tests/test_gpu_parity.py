@@ -109,6 +109,18 @@ def test_chained_layer_beyond_key_cache():
     say(f"  attn max err {res['attn_err']}")
 
 
+def test_chained_layer_at_maximum_batch():
+    """4096 requests (the largest batch the selection and recall kernels take), short ragged
+    contexts: every request's plan, allocation order and attention against the oracle."""
+    rng = np.random.default_rng(4096)
+    ctx = [int(x) for x in rng.integers(1, 160, 4096)]
+    spec, s = W.custom("maxb", ctx, Hq=8, Hkv=2, bs=16, dtype="bf16", k_mid=3, n_sink=1, n_local=1,
+                       resident_frac=0.2, heavy_per_req=1)
+    w, st = build(spec, s)
+    res = full_check(w, st, chained=True)
+    say(f"  {w.B} requests, {res['stats'][0]} recalled blocks, attn max err {res['attn_err']}")
+
+
 def test_select_duplicate_blocks_take_lowest_index():
     """21 exact copies of each request's best middle block compete for 7 places: only the
     lowest-index rule decides, and both sides must pick the same blocks."""
