@@ -186,7 +186,7 @@ PULSE_API pulse_status pulse_select_headwise(const pulse_shape* shape, const voi
  * pass the workspace, B, k_max and total_blocks of the call that planned it
  * (pulse_decode_layer: its total_blocks; pulse_recall_gather and the
  * gather-scatter engine: 0).  A recall that moved no bytes (exhaustion, an
- * error, nothing missing) is not undone; a second release is a no-op.
+ * error, nothing missing) leaves nothing to undo; a second release is a no-op.
  * Stream-ordered, no host sync; inconsistent plans report BAD_INDEX in
  * dev_status.
  */

@@ -189,48 +189,50 @@ __global__ __launch_bounds__(kCopyThreads) void probe_copy_kernel(const uint8_t*
 }
 
 // Step-end release of a recall (undo, LIFO): every block the last recall
-// mapped returns to "not resident" and its slot to the free list.  Phase 1
-// (grid B): clear the table entries of the plan's missing blocks when the
-// recall moved bytes; phase 2 (one thread): give the slots back and clear the
-// statistics, so a second release changes nothing.
-__global__ __launch_bounds__(kCopyThreads) void release_table_kernel(
-    const int32_t* __restrict__ miss_list, const int32_t* __restrict__ miss_cnt, int32_t k_max,
-    int32_t* __restrict__ table, int32_t max_blocks, const pulse_recall_stats* __restrict__ stats, int32_t* status) {
-    if (stats->bytes <= 0) return;
-    const int r = blockIdx.x;
-    int32_t n = miss_cnt[r];
-    if (n < 0 || n > k_max) {
-        if (threadIdx.x == 0) report(status, PULSE_ERR_BAD_INDEX);
-        return;
-    }
-    for (int i = threadIdx.x; i < n; i += kCopyThreads) {
-        const int32_t j = miss_list[(size_t)r * k_max + i];
-        if (j >= 0 && j < max_blocks) table[(size_t)r * max_blocks + j] = -1;
-        else report(status, PULSE_ERR_BAD_INDEX);
-    }
-}
+// mapped returns to "not resident" and its slot to the free list, then the
+// statistics are cleared so a second release changes nothing.  One thread
+// per plan entry (request r, i-th missing block): setting its table entry to
+// -1 is right whether the recall moved the block (it is undone) or not (the
+// entry was still -1), so the table pass needs no statistics; thread 0 alone
+// reads and clears them and moves the free-list head back.
+constexpr int kReleaseThreads = 256;
 
-__global__ void release_head_kernel(int32_t* free_head, pulse_recall_stats* stats, int32_t* status) {
-    if (threadIdx.x != 0 || blockIdx.x != 0 || stats->bytes <= 0) return;
-    if (*free_head < stats->n_missing) {
-        report(status, PULSE_ERR_BAD_INDEX);
-        return;
+__global__ __launch_bounds__(kReleaseThreads) void release_kernel(
+    const int32_t* __restrict__ miss_list, const int32_t* __restrict__ miss_cnt, int32_t B, int32_t k_max,
+    int32_t* __restrict__ table, int32_t max_blocks, int32_t* __restrict__ free_head,
+    pulse_recall_stats* __restrict__ stats, int32_t* status) {
+    const int64_t e = (int64_t)blockIdx.x * kReleaseThreads + threadIdx.x;
+    if (e < (int64_t)B * k_max) {
+        const int32_t r = (int32_t)(e / k_max), i = (int32_t)(e % k_max);
+        const int32_t n = miss_cnt[r];
+        if (n < 0 || n > k_max) {
+            if (i == 0) report(status, PULSE_ERR_BAD_INDEX);
+        } else if (i < n) {
+            const int32_t j = miss_list[(size_t)r * k_max + i];
+            if (j >= 0 && j < max_blocks) table[(size_t)r * max_blocks + j] = -1;
+            else report(status, PULSE_ERR_BAD_INDEX);
+        }
     }
-    *free_head -= stats->n_missing;
-    stats->n_missing = 0;
-    stats->n_runs = 0;
-    stats->bytes = 0;
+    if (e == 0 && stats->bytes > 0) {
+        if (*free_head < stats->n_missing) {
+            report(status, PULSE_ERR_BAD_INDEX);
+        } else {
+            *free_head -= stats->n_missing;
+            stats->n_missing = 0;
+            stats->n_runs = 0;
+            stats->bytes = 0;
+        }
+    }
 }
 
 hipError_t launch_release(const int32_t* miss_list, const int32_t* miss_cnt, int32_t B, int32_t k_max,
                           int32_t* table, int32_t max_blocks, int32_t* free_head, pulse_recall_stats* stats,
                           int32_t* status, hipStream_t st) {
     if (B == 0) return hipSuccess;
-    hipLaunchKernelGGL(release_table_kernel, dim3((unsigned)B), dim3(kCopyThreads), 0, st, miss_list, miss_cnt, k_max,
-                       table, max_blocks, stats, status);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(release_head_kernel, dim3(1), dim3(64), 0, st, free_head, stats, status);
+    const int64_t n = (int64_t)B * k_max;
+    hipLaunchKernelGGL(release_kernel, dim3((unsigned)((n + kReleaseThreads - 1) / kReleaseThreads)),
+                       dim3(kReleaseThreads), 0, st, miss_list, miss_cnt, B, k_max, table, max_blocks, free_head,
+                       stats, status);
     return hipGetLastError();
 }
 
