@@ -292,8 +292,9 @@ PULSE_API pulse_status pulse_recall_gather(const pulse_shape* shape, const void*
  *
  * pulse_gs_engine_create: one engine per device and shape.  Owns a pinned
  *   mailbox for up to max_blocks_per_call plan entries, two pinned and two
- *   device staging buffers of staging_blocks blocks each (double-buffered
- *   batches), an I/O stream, n_workers gather threads and a poller thread.
+ *   device staging buffers of staging_blocks blocks each (batches alternate
+ *   between them), a copy stream for the DMAs and a scatter stream, n_workers
+ *   gather threads and a poller thread.
  *   Allocation happens here, never in the calls below.
  * pulse_gs_recall_submit: same arguments and results as
  *   pulse_recall_gather (set difference, allocation, table / free_head /

@@ -9,9 +9,14 @@
 //                   ready sequence number written to the pinned mailbox)
 //   poller thread:  sees the new sequence number, splits the plan into staging
 //                   batches; worker threads memcpy the blocks from the host
-//                   store into pinned staging (double-buffered);
-//   I/O stream:     one hipMemcpyAsync per batch (staging -> device staging),
-//                   then the scatter kernel (device staging -> pool slots);
+//                   store into pinned staging (two halves; the first batch is
+//                   an eighth of a full one so the link starts early); the
+//                   workers spin while a call is served, so a batch costs no
+//                   thread wake-up;
+//   copy stream:    one hipMemcpyAsync per batch (staging -> device staging),
+//                   back to back;
+//   scatter stream: per batch, after its DMA, the scatter kernel (device
+//                   staging -> pool slots), so no DMA waits for a scatter;
 //   completion:     the poller stores the sequence number as completed; the
 //                   caller polls (semi-synchronous check) or waits with a
 //                   timeout before enqueuing attention.
@@ -146,8 +151,10 @@ struct pulse_gs_engine {
     int32_t* d_slot = nullptr;
     uint8_t* host_stage[2] = {nullptr, nullptr};
     uint8_t* dev_stage[2] = {nullptr, nullptr};
-    hipEvent_t stage_free[2] = {nullptr, nullptr};
-    hipStream_t io = nullptr;
+    hipEvent_t dma_done[2] = {nullptr, nullptr};   // host staging half free again
+    hipEvent_t scat_done[2] = {nullptr, nullptr};  // device staging half free again
+    hipStream_t copy = nullptr;                    // DMAs, back to back
+    hipStream_t scat = nullptr;                    // scatter kernels, each after its DMA
     int device = 0;
     // the call being served
     std::mutex mu;
@@ -168,9 +175,10 @@ struct pulse_gs_engine {
     int n_workers = 0;
     std::vector<std::thread> workers;
     std::mutex wmu;
-    std::condition_variable wcv, wdone;
-    int64_t job_gen = 0;
-    int jobs_left = 0;
+    std::condition_variable wcv;
+    std::atomic<int64_t> job_gen{0};   // bumped (release) once a job's fields are set
+    std::atomic<int> jobs_left{0};      // workers still copying the current job
+    std::atomic<bool> serving{false};   // a call is in progress: idle workers spin, not sleep
     const int64_t* job_src = nullptr;
     uint8_t* job_dst = nullptr;
     int64_t job_n = 0;
@@ -178,37 +186,50 @@ struct pulse_gs_engine {
     void worker_loop(int id) {
         int64_t seen = 0;
         for (;;) {
-            std::unique_lock<std::mutex> lk(wmu);
-            wcv.wait(lk, [&] { return !running.load() || job_gen != seen; });
-            if (job_gen == seen) return;  // stopping with no job pending (a pending job is always drained)
-            seen = job_gen;
+            int64_t g = job_gen.load(std::memory_order_acquire);
+            while (g == seen) {  // wait for the next job
+                if (!running.load()) return;
+                if (serving.load(std::memory_order_relaxed)) {
+                    std::this_thread::yield();
+                } else {
+                    std::unique_lock<std::mutex> lk(wmu);
+                    wcv.wait_for(lk, std::chrono::milliseconds(1), [&] {
+                        return !running.load() || serving.load() || job_gen.load() != seen;
+                    });
+                }
+                g = job_gen.load(std::memory_order_acquire);
+            }
+            seen = g;
             const int64_t n = job_n;
             const int64_t* src = job_src;
             uint8_t* dst = job_dst;
-            lk.unlock();
             const int64_t per = (n + n_workers - 1) / n_workers;
             const int64_t k0 = id * per, k1 = std::min<int64_t>(n, k0 + per);
             for (int64_t k = k0; k < k1; ++k)
                 if (src[k] >= 0) std::memcpy(dst + k * U, cur_host_kv + src[k] * U, U);
-            lk.lock();
-            if (--jobs_left == 0) wdone.notify_one();
+            jobs_left.fetch_sub(1, std::memory_order_acq_rel);
         }
     }
 
+    // All workers copy their share of the n blocks listed in src into dst; returns
+    // when every share is done (spinning: the workers are spinning too).
     void gather(const int64_t* src, uint8_t* dst, int64_t n) {
-        std::unique_lock<std::mutex> lk(wmu);
         job_src = src;
         job_dst = dst;
         job_n = n;
-        jobs_left = n_workers;
-        ++job_gen;
-        wcv.notify_all();
-        wdone.wait(lk, [&] { return jobs_left == 0; });
+        jobs_left.store(n_workers, std::memory_order_relaxed);
+        job_gen.fetch_add(1, std::memory_order_release);
+        while (jobs_left.load(std::memory_order_acquire) != 0) std::this_thread::yield();
     }
 
     void serve(int64_t seq) {
         using clk = std::chrono::steady_clock;
         const auto t0 = clk::now();
+        {
+            std::lock_guard<std::mutex> lk(wmu);  // a worker about to block sees the flag or the notify
+            serving.store(true);
+        }
+        wcv.notify_all();
         {
             std::lock_guard<std::mutex> lk(mu);  // fields of the call, set by the submitting thread
             cur_host_kv = host_kv;
@@ -218,25 +239,42 @@ struct pulse_gs_engine {
         double gather_ms = 0;
         const int64_t n = mb->n_blocks;
         int32_t st = mb->status;
+        // Batches alternate between two staging halves.  The DMAs run back to back on
+        // their own stream; each scatter waits for its DMA on another stream, so a DMA
+        // never waits for the previous scatter.  The first batch is an eighth of a full one
+        // so the link starts early.
         int half = 0;
-        for (int64_t b0 = 0; b0 < n && st == 0; b0 += batch_blocks) {
-            const int64_t nb = std::min<int64_t>(batch_blocks, n - b0);
-            if (hipEventSynchronize(stage_free[half]) != hipSuccess) { st = PULSE_ERR_HIP; break; }
+        for (int64_t b0 = 0, i = 0; b0 < n && st == 0; ++i) {
+            const int64_t want = i == 0 ? std::max<int64_t>(1, batch_blocks / 8) : batch_blocks;
+            const int64_t nb = std::min<int64_t>(want, n - b0);
+            if (hipEventSynchronize(dma_done[half]) != hipSuccess) { st = PULSE_ERR_HIP; break; }
             const auto g0 = clk::now();
             gather(mb_src + b0, host_stage[half], nb);
             gather_ms += std::chrono::duration<double, std::milli>(clk::now() - g0).count();
-            if (hipMemcpyAsync(dev_stage[half], host_stage[half], (size_t)nb * U, hipMemcpyHostToDevice, io) !=
-                hipSuccess) { st = PULSE_ERR_HIP; break; }
-            const int64_t chunks = nb * (int64_t)(U / 16384);
-            hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)std::min<int64_t>(chunks, 1024)), dim3(256), 0, io,
-                               dev_stage[half], d_slot + b0, nb, (int64_t)U, cur_n_slots, cur_pool);
-            if (hipGetLastError() != hipSuccess || hipEventRecord(stage_free[half], io) != hipSuccess) {
+            if (hipStreamWaitEvent(copy, scat_done[half], 0) != hipSuccess ||
+                hipMemcpyAsync(dev_stage[half], host_stage[half], (size_t)nb * U, hipMemcpyHostToDevice, copy) !=
+                    hipSuccess ||
+                hipEventRecord(dma_done[half], copy) != hipSuccess ||
+                hipStreamWaitEvent(scat, dma_done[half], 0) != hipSuccess) {
                 st = PULSE_ERR_HIP;
                 break;
             }
+            const int64_t chunks = nb * (int64_t)(U / 16384);
+            hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)std::min<int64_t>(chunks, 1024)), dim3(256), 0, scat,
+                               dev_stage[half], d_slot + b0, nb, (int64_t)U, cur_n_slots, cur_pool);
+            if (hipGetLastError() != hipSuccess || hipEventRecord(scat_done[half], scat) != hipSuccess) {
+                st = PULSE_ERR_HIP;
+                break;
+            }
+            b0 += nb;
             half ^= 1;
         }
-        if (hipStreamSynchronize(io) != hipSuccess && st == 0) st = PULSE_ERR_HIP;
+        if ((hipStreamSynchronize(copy) != hipSuccess || hipStreamSynchronize(scat) != hipSuccess) && st == 0)
+            st = PULSE_ERR_HIP;
+        {
+            std::lock_guard<std::mutex> lk(wmu);
+            serving.store(false);
+        }
         const auto t1 = clk::now();
         {
             std::lock_guard<std::mutex> lk(mu);
@@ -301,14 +339,18 @@ pulse_status pulse_gs_engine_create(const pulse_shape* shape, int32_t n_workers,
         fail = hipHostMalloc((void**)&e->host_stage[h], (size_t)staging_blocks * e->U, hipHostMallocDefault) !=
                    hipSuccess ||
                hipMalloc((void**)&e->dev_stage[h], (size_t)staging_blocks * e->U) != hipSuccess ||
-               hipEventCreateWithFlags(&e->stage_free[h], hipEventDisableTiming) != hipSuccess;
+               hipEventCreateWithFlags(&e->dma_done[h], hipEventDisableTiming) != hipSuccess ||
+               hipEventCreateWithFlags(&e->scat_done[h], hipEventDisableTiming) != hipSuccess;
     }
-    fail = fail || hipStreamCreateWithFlags(&e->io, hipStreamNonBlocking) != hipSuccess;
+    fail = fail || hipStreamCreateWithFlags(&e->copy, hipStreamNonBlocking) != hipSuccess ||
+           hipStreamCreateWithFlags(&e->scat, hipStreamNonBlocking) != hipSuccess;
+    for (int h = 0; h < 2 && !fail; ++h)
+        fail = hipEventRecord(e->dma_done[h], e->copy) != hipSuccess ||
+               hipEventRecord(e->scat_done[h], e->scat) != hipSuccess;
     if (fail) {
         pulse_gs_engine_destroy(e);
         return PULSE_ERR_HIP;
     }
-    for (int h = 0; h < 2; ++h) (void)hipEventRecord(e->stage_free[h], e->io);
     for (int i = 0; i < n_workers; ++i) e->workers.emplace_back([e, i] { e->worker_loop(i); });
     e->poller = std::thread([e] { e->poll_loop(); });
     *out = e;
@@ -325,12 +367,14 @@ pulse_status pulse_gs_engine_destroy(pulse_gs_engine* e) {
     if (e->poller.joinable()) e->poller.join();
     for (auto& t : e->workers)
         if (t.joinable()) t.join();
-    if (e->io) {
-        (void)hipStreamSynchronize(e->io);
-        (void)hipStreamDestroy(e->io);
-    }
+    for (hipStream_t s : {e->copy, e->scat})
+        if (s) {
+            (void)hipStreamSynchronize(s);
+            (void)hipStreamDestroy(s);
+        }
     for (int h = 0; h < 2; ++h) {
-        if (e->stage_free[h]) (void)hipEventDestroy(e->stage_free[h]);
+        if (e->dma_done[h]) (void)hipEventDestroy(e->dma_done[h]);
+        if (e->scat_done[h]) (void)hipEventDestroy(e->scat_done[h]);
         if (e->host_stage[h]) (void)hipHostFree(e->host_stage[h]);
         if (e->dev_stage[h]) (void)hipFree(e->dev_stage[h]);
     }

@@ -282,7 +282,7 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
         if (result != PULSE_OK) break;
         depths[m] = depth;
         // resume the offload batch: its attention for layer m
-        // (the engine marks a call complete only after its I/O stream has drained)
+        // (the engine marks a call complete only after its streams have drained)
         if ((!engine && hipStreamWaitEvent(irq->cmp, ev_rc1[m], 0) != hipSuccess) ||
             hipEventRecord(ev_att[m], irq->cmp) != hipSuccess || layer_attention(a, irq->cmp) != hipSuccess) {
             result = PULSE_ERR_HIP;
