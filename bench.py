@@ -349,6 +349,7 @@ def bench_layer(cid, args, torch, P, H, W):
         roof["traffic"] = (counter_traffic("recall_copy_kernel") or {}).get("total")
         roof["traffic_split"] = counter_traffic("recall_copy_kernel")
         attn_roof["traffic"] = (counter_traffic("attn_splitk_kernel") or {}).get("total")
+        score_roof["traffic"] = (counter_traffic("score_kernel") or {}).get("total")
     else:
         roof["traffic"] = None
     line = base_line(cid, K, args.warmup)
