@@ -311,7 +311,7 @@ pulse_status pulse_recall_gather(const pulse_shape* shape, const void* host_kv, 
     e = launch_recall_copy(host_kv, blk_off, B, k_max, block_table, max_blocks, free_slots, free_head, n_free,
                            slot_pool, n_slots, pulse_block_bytes(shape), at<int32_t>(ws, w.miss_list),
                            at<int32_t>(ws, w.miss_cnt), at<int32_t>(ws, w.run_cnt), at<int32_t>(ws, w.req_err),
-                           at<int32_t>(ws, w.misc), stats, dev_status, hs);
+                           at<int32_t>(ws, w.misc), stats, dev_status, 8, hs);
     return hip_status(e);
 }
 
@@ -370,13 +370,13 @@ hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mi
 }
 
 // Gather-scatter recall of the plan written by layer_select.
-hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs) {
+hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs, int32_t copy_xcds) {
     const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
     return launch_recall_copy(a.host_kv, a.blk_off, a.B, a.k_max, a.block_table, a.max_blocks, a.free_slots,
                               a.free_head, a.n_free, a.slot_pool, a.n_slots, pulse_block_bytes(&a.shape),
                               at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt),
                               at<int32_t>(a.ws, w.run_cnt), at<int32_t>(a.ws, w.req_err), at<int32_t>(a.ws, w.misc),
-                              a.stats, a.dev_status, hs);
+                              a.stats, a.dev_status, copy_xcds, hs);
 }
 
 // Sparse attention over the selection.

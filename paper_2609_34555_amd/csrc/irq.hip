@@ -8,11 +8,11 @@
 // writes m's sequence number into pinned, host-mapped memory (the "interrupt
 // line": the host reads it without any driver call).  Alternatively the recall
 // goes through the gather-scatter engine (CPU gather, one DMA per batch, GPU
-// scatter), whose completion is host-visible the same way.  On MI355X the
-// engine is the one to pair with IRQ: while the GPU gather kernel streams from
-// host memory, kernels on other streams make little progress (their memory
-// requests wait behind the host reads), so only the DMA path leaves the
-// compute units free for the normal batch.  While that recall is in
+// scatter), whose completion is host-visible the same way.  On MI355X, kernels
+// on other streams make little progress through the XCDs on which a kernel
+// streams from host memory (their memory requests wait behind the host reads),
+// so here the gather kernel copies from one XCD only; the engine's DMA leaves
+// every XCD to the normal batch.  While that recall is in
 // flight the host keeps enqueuing normal-batch layers on the compute stream
 // and, at each normal layer boundary, checks the flag.  Once it is set, the
 // offload batch's attention for layer m is enqueued on the compute stream
@@ -67,6 +67,11 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const __bf16* __restrict__ 
         h[i] = (__bf16)(g / (1.f + expf(-g)) * u);
     }
 }
+
+// The gather kernel copies from one XCD while normal-batch layers run: the link rate
+// holds and the other XCDs keep serving HBM (from all XCDs, the concurrent layers
+// would barely progress until the recall ends).
+constexpr int32_t kIrqRecallXcds = 1;
 
 static unsigned grid_for(int64_t n) {
     int64_t g = (n + 255) / 256;
@@ -248,7 +253,8 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
         } else {
             seq = ++irq->seq;
             if (hipStreamWaitEvent(irq->io, ev_sel[m], 0) != hipSuccess ||
-                hipEventRecord(ev_rc0[m], irq->io) != hipSuccess || layer_recall(a, irq->io) != hipSuccess) {
+                hipEventRecord(ev_rc0[m], irq->io) != hipSuccess ||
+                layer_recall(a, irq->io, kIrqRecallXcds) != hipSuccess) {
                 result = PULSE_ERR_HIP;
                 break;
             }

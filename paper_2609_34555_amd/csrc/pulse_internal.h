@@ -118,7 +118,7 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
                               int32_t* free_head, int32_t n_free, void* pool, int32_t n_slots,
                               size_t unit_bytes, const int32_t* miss_list, const int32_t* miss_cnt,
                               const int32_t* run_cnt, const int32_t* req_err, const int32_t* misc,
-                              pulse_recall_stats* stats, int32_t* status, hipStream_t st);
+                              pulse_recall_stats* stats, int32_t* status, int32_t copy_xcds, hipStream_t st);
 
 hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
                             const int32_t* table, int32_t max_blocks, const int32_t* sel_idx,
@@ -148,7 +148,7 @@ inline T* ws_at(void* ws, size_t off) {
 // Stages of a chained layer-step (api.hip): score + select + plan, recall,
 // attention; and the full argument check of pulse_layer_args.
 hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mid);
-hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs);
+hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs, int32_t copy_xcds = 8);
 hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs);
 pulse_status check_layer_args(const pulse_layer_args* a);
 

@@ -30,6 +30,12 @@ namespace pulse {
 constexpr int kPlanThreads = 256;
 constexpr int kCopyThreads = 256;
 constexpr int64_t kRecallGrid = PULSE_RECALL_GRID;  // persistent copy workgroups
+// Workgroups are dispatched to the 8 XCDs round-robin by id.  While a kernel reads
+// pinned host memory, other kernels' HBM traffic through the same XCDs waits behind
+// it.  With copy_xcds < 8 only the workgroups on the first copy_xcds XCDs copy: one
+// XCD's 16 workgroups still reach the link rate, and the other XCDs stay free for
+// concurrent kernels (which then also take a little link bandwidth); with 8, all do.
+constexpr int kXcds = 8;
 constexpr int kMaxBatch = 4096;  // requests per call supported by the copy kernel
 
 __device__ inline uint64_t lanemask_lt_r() {
@@ -117,7 +123,7 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     int32_t* __restrict__ free_head, int32_t n_free, uint8_t* __restrict__ pool, int32_t n_slots, int64_t U,
     const int32_t* __restrict__ miss_list, const int32_t* __restrict__ miss_cnt,
     const int32_t* __restrict__ run_cnt, const int32_t* __restrict__ req_err, const int32_t* __restrict__ misc,
-    pulse_recall_stats* __restrict__ stats, int32_t* status) {
+    pulse_recall_stats* __restrict__ stats, int32_t* status, int32_t copy_xcds) {
     __shared__ int32_t off[kMaxBatch + 1];
     __shared__ uint32_t part_sum[kCopyThreads];
     __shared__ uint32_t sh_runs, sh_bad;
@@ -159,7 +165,14 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     constexpr int64_t chunk = 4096 * LPT;
     const int64_t cpb = U / chunk;
     const int64_t n_chunks = total * cpb;
-    for (int64_t c = blockIdx.x; c < n_chunks; c += gridDim.x) {
+    // copying workgroups: those on the first copy_xcds XCDs when the grid spans whole
+    // rounds of kXcds, else all
+    const bool confine = copy_xcds >= 1 && copy_xcds < kXcds && gridDim.x % kXcds == 0;
+    const int xcd = (int)(blockIdx.x % kXcds);
+    if (confine && xcd >= copy_xcds) return;
+    const int64_t c0 = confine ? (int64_t)(blockIdx.x / kXcds) * copy_xcds + xcd : (int64_t)blockIdx.x;
+    const int64_t cstride = confine ? (int64_t)(gridDim.x / kXcds) * copy_xcds : (int64_t)gridDim.x;
+    for (int64_t c = c0; c < n_chunks; c += cstride) {
         const int64_t g = c / cpb;
         const int64_t part = c - g * cpb;
         int lo = 0, hi = B;  // largest r with off[r] <= g
@@ -250,7 +263,8 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
                               int32_t max_blocks, const int32_t* free_slots, int32_t* free_head, int32_t n_free,
                               void* pool, int32_t n_slots, size_t unit_bytes, const int32_t* miss_list,
                               const int32_t* miss_cnt, const int32_t* run_cnt, const int32_t* req_err,
-                              const int32_t* misc, pulse_recall_stats* stats, int32_t* status, hipStream_t st) {
+                              const int32_t* misc, pulse_recall_stats* stats, int32_t* status, int32_t copy_xcds,
+                              hipStream_t st) {
     if (B == 0) return hipSuccess;
     // 16-byte loads in flight per thread: the largest of PULSE_RECALL_LPT, 4, 2 whose
     // 4 KiB * LPT chunk divides the block
@@ -263,7 +277,7 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
 #define PULSE_COPY(L)                                                                                            \
     hipLaunchKernelGGL(recall_copy_kernel<L>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,    \
                        blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool, n_slots, \
-                       (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status)
+                       (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status, copy_xcds)
     if (lpt == 8) PULSE_COPY(8);
     else if (lpt == 4) PULSE_COPY(4);
     else PULSE_COPY(2);
