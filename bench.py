@@ -174,9 +174,76 @@ def engine_recall_baseline(torch, P, st, w, reps=5):
             "staging_MiB": 16}
 
 
+def host_info():
+    """CPU model, logical CPUs usable by this process and installed memory of this host."""
+    info = {"nproc": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
+    try:
+        with open("/proc/cpuinfo") as f:
+            info["model"] = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+        with open("/proc/meminfo") as f:
+            kb = next(int(ln.split()[1]) for ln in f if ln.startswith("MemTotal"))
+        info["mem_GiB"] = round(kb / 2**20, 1)
+    except (OSError, StopIteration, ValueError):
+        pass
+    return info
+
+
+def _oracle_step(O, w, dig, host, pool, table, pool_u16, threads, pool_exec):
+    """One layer-step through the oracle, returning its stage times (s), recall stats and
+    attention output.  With a thread pool the per-request stages (score, select,
+    attention) run one request per task -- the oracle's C calls release the GIL -- and
+    the recall, whose slot allocation follows the global request order, runs whole."""
+    import numpy as np
+
+    t = [time.perf_counter()]
+    if pool_exec is None:
+        sc = O.score(w.q, dig, w.blk_off, w.Hq, w.Hkv, w.d, w.dtype_code, w.solo_kv_head)
+        t.append(time.perf_counter())
+        rc, idx, cnt = O.select(sc, w.blk_off, w.k_mid, w.n_sink, w.n_local, w.k_max)
+    else:
+        offs = w.blk_off.tolist()
+
+        def score_select(r):
+            lo, hi = offs[r], offs[r + 1]
+            one = np.array([0, hi - lo], np.int64)
+            s_r = O.score(w.q[r:r + 1], dig[lo:hi], one, w.Hq, w.Hkv, w.d, w.dtype_code, w.solo_kv_head)
+            return O.select(s_r, one, w.k_mid[r:r + 1], w.n_sink, w.n_local, w.k_max)
+
+        parts = list(pool_exec.map(score_select, range(w.B)))
+        rc = max(p[0] for p in parts)
+        idx = np.concatenate([p[1] for p in parts])
+        cnt = np.concatenate([p[2] for p in parts])
+    t.append(time.perf_counter())
+    rc2, fh, stats = O.recall(host, w.blk_off, idx, cnt, table, w.free_slots, 0, pool, w.unit_bytes)
+    t.append(time.perf_counter())
+    if pool_exec is None:
+        out, lse = O.attention(w.q, pool_u16, table, idx, cnt, w.blk_off, w.ctx_len, w.Hq, w.Hkv, w.bs, w.d,
+                               w.dtype_code, w.sm_scale)
+    else:
+        def attend(r):
+            one = np.array([0, offs[r + 1] - offs[r]], np.int64)
+            return O.attention(w.q[r:r + 1], pool_u16, table[r:r + 1], idx[r:r + 1], cnt[r:r + 1], one,
+                               w.ctx_len[r:r + 1], w.Hq, w.Hkv, w.bs, w.d, w.dtype_code, w.sm_scale)
+
+        res = list(pool_exec.map(attend, range(w.B)))
+        out = np.concatenate([o for o, _ in res])
+        lse = np.concatenate([l for _, l in res])
+    t.append(time.perf_counter())
+    if rc or rc2:
+        raise RuntimeError(f"oracle status {rc} / {rc2}")
+    dt = [b - a for a, b in zip(t, t[1:])]
+    names = ["score", "select", "recall", "attention"] if pool_exec is None else \
+        ["score+select", "recall", "attention"]  # one task per request covers both
+    return dict(zip(names, dt)), stats, out, lse
+
+
 def cpu_baseline(w, seconds, sample_note="whole layer-steps of the same workload"):
-    """The CPU oracle timed on this host, single thread, on whole layer-steps of the same
-    workload (digests are per-block state, built once outside the timing)."""
+    """The CPU oracle timed on this host on whole layer-steps of the same workload (digests
+    are per-block state, built once outside the timing): single thread, then -- over
+    requests, on up to 16 threads -- the same oracle calls one request at a time.  Both
+    modes' outputs are checked to be identical."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import numpy as np
 
     from oracle import pulse_oracle as O
@@ -185,23 +252,44 @@ def cpu_baseline(w, seconds, sample_note="whole layer-steps of the same workload
     dig = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, w.solo_kv_head)
     pool0 = W.initial_pool(w).view(np.uint8).reshape(w.n_slots, -1)
     host = w.kv.view(np.uint8).reshape(w.total_blocks, -1)
-    elapsed, steps, nbytes = 0.0, 0, 0
-    while elapsed < seconds or steps < 2:
-        table = w.table0.copy()
-        pool = pool0.copy()
-        t0 = time.perf_counter()
-        sc = O.score(w.q, dig, w.blk_off, w.Hq, w.Hkv, w.d, w.dtype_code, w.solo_kv_head)
-        rc, idx, cnt = O.select(sc, w.blk_off, w.k_mid, w.n_sink, w.n_local, w.k_max)
-        rc2, fh, stats = O.recall(host, w.blk_off, idx, cnt, table, w.free_slots, 0, pool, w.unit_bytes)
-        O.attention(w.q, pool.view(np.uint16).reshape(w.n_slots, -1), table, idx, cnt, w.blk_off, w.ctx_len, w.Hq,
-                    w.Hkv, w.bs, w.d, w.dtype_code, w.sm_scale)
-        elapsed += time.perf_counter() - t0
-        steps += 1
-        nbytes = stats[2]
-    per_step = elapsed / steps
-    return {"value": nbytes / per_step / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{steps} x {sample_note} ({w.B} requests), single thread",
-            "us_per_layer_step": per_step * 1e6}
+
+    def run(threads, budget):
+        ex = ThreadPoolExecutor(threads) if threads > 1 else None
+        stage = {}
+        steps, nbytes, first = 0, 0, None
+        try:
+            while sum(stage.values()) < budget or steps < 2:
+                table = w.table0.copy()
+                pool = pool0.copy()
+                pool_u16 = pool.view(np.uint16).reshape(w.n_slots, -1)
+                dt, stats, out, lse = _oracle_step(O, w, dig, host, pool, table, pool_u16, threads, ex)
+                for k, v in dt.items():
+                    stage[k] = stage.get(k, 0.0) + v
+                steps += 1
+                nbytes = stats[2]
+                if first is None:
+                    first = (out, lse)
+        finally:
+            if ex is not None:
+                ex.shutdown()
+        per_step = sum(stage.values()) / steps
+        return {"value": nbytes / per_step / 1e9, "unit": "GB/s", "cores": threads, "steps": steps,
+                "us_per_layer_step": per_step * 1e6,
+                "stage_us": {k: v / steps * 1e6 for k, v in stage.items()}}, first
+
+    single, ref = run(1, seconds)
+    line = {"kind": "oracle", **single,
+            "sample": f"{single['steps']} x {sample_note} ({w.B} requests), single thread",
+            "host": host_info()}
+    threads = min(16, line["host"]["usable_cpus"], w.B)
+    if threads > 1:
+        par, got = run(threads, seconds / 2)
+        if not (np.array_equal(got[0], ref[0]) and np.array_equal(got[1], ref[1])):
+            raise RuntimeError("threaded oracle run differs from the single-thread run")
+        par["sample"] = (f"{par['steps']} x the same layer-steps, one request per task on {threads} threads "
+                         "(score + select and attention per request; recall whole)")
+        line["threaded"] = par
+    return line
 
 
 WORKLOADS = {
@@ -260,7 +348,7 @@ def timed_steps(torch, P, st, K, warmup):
         stage["attention"].append(e.elapsed_ms(3, 4))
         stage["layer"].append(e.elapsed_ms(0, 4))
         e.destroy()
-    return wall, {k: statistics.mean(v) for k, v in stage.items()}
+    return wall, {k: statistics.mean(v) for k, v in stage.items()}, {k: statistics.median(v) for k, v in stage.items()}
 
 
 def hbm_probe(torch, P, nbytes, reps=10):
@@ -284,6 +372,39 @@ def hbm_probe(torch, P, nbytes, reps=10):
     ms = statistics.mean(e0.elapsed_time(e1) for e0, e1 in evs)
     del src, sink
     return nbytes / (ms * 1e-3) / 1e9
+
+
+def attention_warm_cold(torch, st, attn_bytes, reps=10):
+    """The attention call (split-K kernel + combine) alone, warm and cold.  In the chained
+    step the recall has just written part of the selected blocks, and a working set under
+    256 MB can stay in the Infinity Cache: warm launches repeat the call on the same
+    selection; cold ones first read 1 GiB of other data, which evicts the working set
+    without leaving dirty lines to write back.  HIP events bracket each launch on the
+    current stream; mean over `reps` launches."""
+    scratch = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+    res = {}
+    for mode in ("warm", "cold"):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        sink = []
+        st.attention()
+        torch.cuda.synchronize()
+        torch.cuda._sleep(20_000_000)  # keeps the GPU busy while the launches below are enqueued
+        for e0, e1 in evs:
+            if mode == "cold":
+                sink.append(scratch.sum())
+            else:
+                st.attention()
+            e0.record()
+            st.attention()
+            e1.record()
+        torch.cuda.synchronize()
+        ms = statistics.mean(e0.elapsed_time(e1) for e0, e1 in evs)
+        res[mode] = {"us": ms * 1e3, "GBps": attn_bytes / (ms * 1e-3) / 1e9,
+                     "frac": attn_bytes / (ms * 1e-3) / 1e9 / HBM_GBPS}
+    del scratch
+    if st.status() != 0:
+        raise RuntimeError(f"device status {st.status()} after the isolated attention runs")
+    return res
 
 
 def rooflines(w, st, mean, rbytes, peak_measured):
@@ -313,7 +434,7 @@ def bench_layer(cid, args, torch, P, H, W):
     st = H.LayerState(w, holder[0].ptr)
     torch.cuda.synchronize()
     K = args.steps
-    wall, mean = timed_steps(torch, P, st, K, args.warmup)
+    wall, mean, median = timed_steps(torch, P, st, K, args.warmup)
     status = st.status()
     if status != 0:
         raise RuntimeError(f"device status {P.status_string(status)}")
@@ -345,6 +466,7 @@ def bench_layer(cid, args, torch, P, H, W):
             r["peak_measured"] = hbm_probe(torch, P, r["bytes_per_launch"])
             r["frac_of_measured"] = r["achieved"] / r["peak_measured"]
         extras["hbm_read_1GiB_GBps"] = hbm_probe(torch, P, 1 << 30)
+        attn_roof["isolated"] = attention_warm_cold(torch, st, attn_roof["bytes_per_launch"])
     if cid == 2:  # the committed counter passes were taken on this workload
         roof["traffic"] = (counter_traffic("recall_copy_kernel") or {}).get("total")
         roof["traffic_split"] = counter_traffic("recall_copy_kernel")
@@ -362,6 +484,7 @@ def bench_layer(cid, args, torch, P, H, W):
         "recall": {"bytes_per_step": rbytes, "blocks": n_missing, "runs": n_runs,
                    "kernel_GBps": roof["achieved"]},
         "stage_us": {k: v * 1e3 for k, v in mean.items()},
+        "stage_us_median": {k: v * 1e3 for k, v in median.items()},
         "roofline": roof,
         "roofline_hbm_attention": attn_roof,
         "roofline_hbm_score": score_roof,

@@ -93,7 +93,19 @@ __device__ inline float dot2(uint32_t a, uint32_t b, float acc) {
         return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, a), __builtin_bit_cast(f16x2, b), acc, false);
 }
 
-constexpr int kScoreBlocksPerWg = 64;  // 16 groups x 4 iterations
+// Two shapes of the score kernel, chosen by the number of digests read:
+// small sets (up to kScoreLargeBlocks) take one 16-block iteration per
+// workgroup, so more workgroups share the short stream; large ones take two
+// iterations with non-temporal loads, which keep the once-read digests from
+// displacing cached lines.  Both measured faster than the other's setting at
+// their sizes (and than 4 or more iterations, or a grid-stride form).
+constexpr int64_t kScoreLargeBlocks = 65536;
+
+template <bool NT>
+__device__ inline u32x4 score_load(const u32x4* p) {
+    if constexpr (NT) return __builtin_nontemporal_load(p);
+    return *p;
+}
 
 // Largest r in [0, B) with off[r] <= b, over an LDS copy of blk_off.
 __device__ inline int find_request_lds(const int64_t* off, int32_t B, int64_t b) {
@@ -110,7 +122,7 @@ __device__ inline int find_request_lds(const int64_t* off, int32_t B, int64_t b)
 // blockIdx.y selects the scoring KV head when several heads score at once
 // (headwise selection); with one head it is `solo`.  blk_off is staged in LDS
 // so the request of a block costs no dependent global loads.
-template <int DT, int G>
+template <int DT, int G, int ITERS, bool NT>
 __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__ q,
                                                     const uint16_t* __restrict__ digests,
                                                     const int64_t* __restrict__ blk_off, int32_t B,
@@ -123,16 +135,16 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
     const int sub = threadIdx.x & 15;
     const int gi = threadIdx.x >> 4;
     const int c8 = sub * 8;
-    const int64_t base = (int64_t)blockIdx.x * kScoreBlocksPerWg + gi;
+    const int64_t base = (int64_t)blockIdx.x * (16 * ITERS) + gi;
     // digest loads first: their addresses do not depend on the request
-    u32x4 dmn[4], dmx[4];
+    u32x4 dmn[ITERS], dmx[ITERS];
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < ITERS; ++it) {
         const int64_t b = base + 16 * it;
         if (b < total_blocks) {
             const u32x4* dg = reinterpret_cast<const u32x4*>(digests + (size_t)b * 2 * kHeadDim);
-            dmn[it] = dg[sub];
-            dmx[it] = dg[16 + sub];
+            dmn[it] = score_load<NT>(dg + sub);
+            dmx[it] = score_load<NT>(dg + 16 + sub);
         }
     }
     for (int i = threadIdx.x; i <= B; i += 256) s_off[i] = blk_off[i];
@@ -141,7 +153,7 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
     int64_t r_lo = 0, r_hi = 0;
     uint32_t qp[G][4], qm[G][4];
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < ITERS; ++it) {
         const int64_t b = base + 16 * it;
         if (b >= total_blocks) break;
         if (b >= r_hi || b < r_lo) {
@@ -189,20 +201,27 @@ hipError_t launch_build_digests(const pulse_shape& s, const void* kv, const int6
 }
 
 template <int DT, int G>
-static void launch_score_t(dim3 grid, hipStream_t st, const void* q, const void* digests, const int64_t* blk_off,
+static void launch_score_t(int32_t heads, hipStream_t st, const void* q, const void* digests, const int64_t* blk_off,
                            int32_t B, int64_t total, int32_t Hq, int32_t solo, int32_t n_sink, int32_t n_local,
                            float* scores) {
     const size_t lds = sizeof(int64_t) * ((size_t)B + 1);
-    hipLaunchKernelGGL((score_kernel<DT, G>), grid, dim3(256), lds, st, (const uint16_t*)q,
-                       (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores);
+    if (total * heads > kScoreLargeBlocks) {
+        const dim3 grid((unsigned)((total + 31) / 32), (unsigned)heads);
+        hipLaunchKernelGGL((score_kernel<DT, G, 2, true>), grid, dim3(256), lds, st, (const uint16_t*)q,
+                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores);
+    } else {
+        const dim3 grid((unsigned)((total + 15) / 16), (unsigned)heads);
+        hipLaunchKernelGGL((score_kernel<DT, G, 1, false>), grid, dim3(256), lds, st, (const uint16_t*)q,
+                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores);
+    }
 }
 
 template <int DT>
-static void launch_score_dt(int G, dim3 grid, hipStream_t st, const void* q, const void* digests,
+static void launch_score_dt(int G, int32_t heads, hipStream_t st, const void* q, const void* digests,
                             const int64_t* blk_off, int32_t B, int64_t total, int32_t Hq, int32_t solo,
                             int32_t n_sink, int32_t n_local, float* scores) {
 #define PULSE_SCORE_CASE(g) \
-    case g: launch_score_t<DT, g>(grid, st, q, digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores); break;
+    case g: launch_score_t<DT, g>(heads, st, q, digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores); break;
     switch (G) {
         PULSE_SCORE_CASE(1) PULSE_SCORE_CASE(2) PULSE_SCORE_CASE(3) PULSE_SCORE_CASE(4)
         PULSE_SCORE_CASE(5) PULSE_SCORE_CASE(6) PULSE_SCORE_CASE(7) PULSE_SCORE_CASE(8)
@@ -218,12 +237,11 @@ hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests
                         float* scores, int32_t heads, hipStream_t st) {
     if (total_blocks == 0) return hipSuccess;
     const int G = s.num_q_heads / s.num_kv_heads;
-    dim3 grid((unsigned)((total_blocks + kScoreBlocksPerWg - 1) / kScoreBlocksPerWg), (unsigned)heads);
     if (s.dtype == PULSE_BF16)
-        launch_score_dt<PULSE_BF16>(G, grid, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
+        launch_score_dt<PULSE_BF16>(G, heads, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
                                     n_local, scores);
     else
-        launch_score_dt<PULSE_F16>(G, grid, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
+        launch_score_dt<PULSE_F16>(G, heads, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
                                    n_local, scores);
     return hipGetLastError();
 }

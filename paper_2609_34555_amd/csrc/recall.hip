@@ -16,6 +16,8 @@
 // Copy kernel (persistent grid): every workgroup scans the per-request
 // counts (small), checks the pool capacity, then copies 4 KiB * LPT chunks;
 // the chunk that starts a block also writes its block-table entry.
+#include <type_traits>
+
 #include "pulse_internal.h"
 
 namespace pulse {
@@ -106,14 +108,26 @@ __global__ __launch_bounds__(kPlanThreads) void recall_plan_kernel(
     }
 }
 
-template <int LPT>
+// Recalls larger than this (the 256 MB Infinity Cache) are stored non-temporally:
+// such a volume cannot stay cached until the attention reads it, and storing it
+// through keeps its write-back out of the attention that follows (measured: the
+// attention after a 490 MB recall 13% faster; after recalls of 57-170 MB, which
+// partly stay cached, normal stores are 3-8% better for it).
+constexpr int64_t kNtStoreBytes = (int64_t)256 << 20;
+
+template <int LPT, bool NT>
 __device__ inline void copy_chunk(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst, int tid) {
     u32x4 v[LPT];
 #pragma unroll
     for (int k = 0; k < LPT; ++k)
         v[k] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src) + tid + k * kCopyThreads);
 #pragma unroll
-    for (int k = 0; k < LPT; ++k) reinterpret_cast<u32x4*>(dst)[tid + k * kCopyThreads] = v[k];
+    for (int k = 0; k < LPT; ++k) {
+        if constexpr (NT)
+            __builtin_nontemporal_store(v[k], reinterpret_cast<u32x4*>(dst) + tid + k * kCopyThreads);
+        else
+            reinterpret_cast<u32x4*>(dst)[tid + k * kCopyThreads] = v[k];
+    }
 }
 
 template <int LPT>
@@ -165,6 +179,7 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     constexpr int64_t chunk = 4096 * LPT;
     const int64_t cpb = U / chunk;
     const int64_t n_chunks = total * cpb;
+    const bool nt_store = total * U > kNtStoreBytes;
     // copying workgroups: those on the first copy_xcds XCDs when the grid spans whole
     // rounds of kXcds, else all
     const bool confine = copy_xcds >= 1 && copy_xcds < kXcds && gridDim.x % kXcds == 0;
@@ -172,33 +187,40 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     if (confine && xcd >= copy_xcds) return;
     const int64_t c0 = confine ? (int64_t)(blockIdx.x / kXcds) * copy_xcds + xcd : (int64_t)blockIdx.x;
     const int64_t cstride = confine ? (int64_t)(gridDim.x / kXcds) * copy_xcds : (int64_t)gridDim.x;
-    for (int64_t c = c0; c < n_chunks; c += cstride) {
-        const int64_t g = c / cpb;
-        const int64_t part = c - g * cpb;
-        int lo = 0, hi = B;  // largest r with off[r] <= g
-        while (hi - lo > 1) {
-            const int mid = (lo + hi) >> 1;
-            if (off[mid] <= g) lo = mid; else hi = mid;
+    // one loop per store kind, so the compiler cannot merge the two kinds of stores
+    auto copy_all = [&](auto nt) {
+        for (int64_t c = c0; c < n_chunks; c += cstride) {
+            const int64_t g = c / cpb;
+            const int64_t part = c - g * cpb;
+            int lo = 0, hi = B;  // largest r with off[r] <= g
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (off[mid] <= g) lo = mid; else hi = mid;
+            }
+            const int r = lo;
+            const int32_t j = miss_list[(size_t)r * k_max + (g - off[r])];
+            const int32_t slot = free_slots[fh0 + g];
+            if (slot < 0 || slot >= n_slots) {
+                if (tid == 0 && part == 0) report(status, PULSE_ERR_BAD_INDEX);
+                continue;
+            }
+            const uint8_t* src = host + (blk_off[r] + j) * U + part * chunk;
+            uint8_t* dst = pool + (int64_t)slot * U + part * chunk;
+            copy_chunk<LPT, decltype(nt)::value>(src, dst, tid);
+            if (part == 0 && tid == 0) table[(size_t)r * max_blocks + j] = slot;
         }
-        const int r = lo;
-        const int32_t j = miss_list[(size_t)r * k_max + (g - off[r])];
-        const int32_t slot = free_slots[fh0 + g];
-        if (slot < 0 || slot >= n_slots) {
-            if (tid == 0 && part == 0) report(status, PULSE_ERR_BAD_INDEX);
-            continue;
-        }
-        const uint8_t* src = host + (blk_off[r] + j) * U + part * chunk;
-        uint8_t* dst = pool + (int64_t)slot * U + part * chunk;
-        copy_chunk<LPT>(src, dst, tid);
-        if (part == 0 && tid == 0) table[(size_t)r * max_blocks + j] = slot;
-    }
+    };
+    if (nt_store)
+        copy_all(std::true_type{});
+    else
+        copy_all(std::false_type{});
 }
 
 // streaming host -> device copy with the load pattern of the recall kernel
 __global__ __launch_bounds__(kCopyThreads) void probe_copy_kernel(const uint8_t* __restrict__ src,
                                                                  uint8_t* __restrict__ dst, int64_t n_chunks) {
     for (int64_t c = blockIdx.x; c < n_chunks; c += gridDim.x)
-        copy_chunk<4>(src + c * 16384, dst + c * 16384, threadIdx.x);
+        copy_chunk<4, false>(src + c * 16384, dst + c * 16384, threadIdx.x);
 }
 
 // Step-end release of a recall (undo, LIFO): every block the last recall

@@ -1,0 +1,39 @@
+"""Host logic of the benchmark's CPU baseline: the threaded mode runs the oracle one request
+at a time and must reproduce the whole-batch oracle step exactly (selection, recall
+statistics, table, pool bytes, attention output)."""
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+import bench
+from oracle import pulse_oracle as O
+from paper_2609_34555_amd import workloads as W
+
+
+def _step(w, ex):
+    dig = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, w.solo_kv_head)
+    pool = W.initial_pool(w).view(np.uint8).reshape(w.n_slots, -1).copy()
+    host = w.kv.view(np.uint8).reshape(w.total_blocks, -1)
+    table = w.table0.copy()
+    dt, stats, out, lse = bench._oracle_step(O, w, dig, host, pool, table, pool.view(np.uint16).reshape(w.n_slots, -1),
+                                             4 if ex else 1, ex)
+    return dt, stats, out, lse, table, pool
+
+
+def test_threaded_oracle_step_matches_whole_batch():
+    spec, seed = W.custom("ragged", [1000, 37, 4096, 517, 16], k_mid=[6, 1, 20, 9, 3], n_local=2,
+                          resident_frac=0.2, heavy_per_req=3)
+    w = W.generate(spec, seed)
+    dt1, st1, out1, lse1, tab1, pool1 = _step(w, None)
+    with ThreadPoolExecutor(4) as ex:
+        dt4, st4, out4, lse4, tab4, pool4 = _step(w, ex)
+    assert set(dt1) == {"score", "select", "recall", "attention"}
+    assert set(dt4) == {"score+select", "recall", "attention"}
+    assert st1 == st4 and st1[0] > 0
+    assert np.array_equal(tab1, tab4) and np.array_equal(pool1, pool4)
+    assert np.array_equal(out1, out4) and np.array_equal(lse1, lse4)
+
+
+def test_host_info_fields():
+    info = bench.host_info()
+    assert info["nproc"] >= 1 and 1 <= info["usable_cpus"] <= info["nproc"]
