@@ -314,41 +314,58 @@ def base_line(cid, K, warmup):
             "data": "synthetic (seeded N(0,1) K/V/q, planted heavy blocks; no model weights or datasets)"}
 
 
-def timed_steps(torch, P, st, K, warmup):
-    """W untimed steps, then exactly K timed steps (pulse_decode_layer + pulse_release_recalled),
-    bracketed by device synchronisation; per-stage HIP events of every step are read
-    after the timed region."""
+def _event_pass(torch, P, st, K, keep):
+    """K steps whose layer-steps record the stage events in `keep` (indices into the five
+    of pulse_layer_args.events; the others are left out).  Returns the EventSets and the
+    host wall time of the K steps."""
     evs = [P.EventSet(5) for _ in range(K)]
-    plain = st.layer_args()
-    timed = []
+    args = []
     for e in evs:
         a = st.layer_args()
-        a.events = e.ptr
-        timed.append(a)
+        a.events = e.masked_ptr(keep)
+        args.append(a)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for a in args:
+        P.pulse_decode_layer(a)
+        st.release(chained=True)
+    torch.cuda.synchronize()
+    return evs, time.perf_counter() - t0
+
+
+def timed_steps(torch, P, st, K, warmup):
+    """W untimed steps, then exactly K timed steps (pulse_decode_layer + pulse_release_recalled),
+    bracketed by device synchronisation.  Inside the timed region only the two events around
+    the recall copy (the roofline kernel) are recorded: each record adds ~3 us to the stream.
+    Two untimed passes of K steps follow: events before score and after attention only (the
+    chain's duration), then all five (the per-stage split, which carries the records' cost)."""
+    plain = st.layer_args()
     # a step = the layer-step plus the step-end release of its recall (the hot set stays
     # fixed-size), so every step recalls the same blocks; state is reset once, untimed
     st.reset()
     for _ in range(warmup):
         P.pulse_decode_layer(plain)
         st.release(chained=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for a in timed:
-        P.pulse_decode_layer(a)
-        st.release(chained=True)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    evs, wall = _event_pass(torch, P, st, K, (2, 3))  # the timed region
+    recall = [e.elapsed_ms(2, 3) for e in evs]
+    chain_evs, _ = _event_pass(torch, P, st, K, (0, 4))
+    layer = [e.elapsed_ms(0, 4) for e in chain_evs]
+    stage_evs, _ = _event_pass(torch, P, st, K, (0, 1, 2, 3, 4))
     P.pulse_decode_layer(plain)  # untimed: leaves this step's recall statistics and tables in place
     torch.cuda.synchronize()
     stage = {"score": [], "select": [], "recall": [], "attention": [], "layer": []}
-    for e in evs:
+    for e in stage_evs:
         stage["score"].append(e.elapsed_ms(0, 1))
         stage["select"].append(e.elapsed_ms(1, 2))
         stage["recall"].append(e.elapsed_ms(2, 3))
         stage["attention"].append(e.elapsed_ms(3, 4))
         stage["layer"].append(e.elapsed_ms(0, 4))
+    for e in evs + chain_evs + stage_evs:
         e.destroy()
-    return wall, {k: statistics.mean(v) for k, v in stage.items()}, {k: statistics.median(v) for k, v in stage.items()}
+    timed = {"recall": statistics.mean(recall), "layer": statistics.mean(layer),
+             "layer_median": statistics.median(layer)}
+    return (wall, timed, {k: statistics.mean(v) for k, v in stage.items()},
+            {k: statistics.median(v) for k, v in stage.items()})
 
 
 def hbm_probe(torch, P, nbytes, reps=10):
@@ -407,8 +424,10 @@ def attention_warm_cold(torch, st, attn_bytes, reps=10):
     return res
 
 
-def rooflines(w, st, mean, rbytes, peak_measured):
-    recall_GBps = rbytes / (mean["recall"] * 1e-3) / 1e9
+def rooflines(w, st, timed, mean, rbytes, peak_measured):
+    """The recall's rate from the timed region's events; attention and score from the
+    all-stage pass."""
+    recall_GBps = rbytes / (timed["recall"] * 1e-3) / 1e9
     sel = st.sel_cnt.cpu().numpy()
     attn_bytes = int(sel.sum()) * w.unit_bytes + w.q.nbytes + w.B * w.Hq * w.d * 4
     digest_bytes = int(sum(max(0, n - w.n_sink - w.n_local) for n in w.n_blocks.tolist())) * 2 * w.d * 2
@@ -434,7 +453,7 @@ def bench_layer(cid, args, torch, P, H, W):
     st = H.LayerState(w, holder[0].ptr)
     torch.cuda.synchronize()
     K = args.steps
-    wall, mean, median = timed_steps(torch, P, st, K, args.warmup)
+    wall, timed, mean, median = timed_steps(torch, P, st, K, args.warmup)
     status = st.status()
     if status != 0:
         raise RuntimeError(f"device status {P.status_string(status)}")
@@ -460,7 +479,7 @@ def bench_layer(cid, args, torch, P, H, W):
         extras["paper_engine_recall"] = engine_recall_baseline(torch, P, st, w)
     peak_measured = max([extras["link"]["memcpy_1GiB_GBps"], extras["link"]["kernel_read_1GiB_GBps"]]
                         if "link" in extras else [0.0]) or None
-    roof, attn_roof, score_roof = rooflines(w, st, mean, rbytes, peak_measured)
+    roof, attn_roof, score_roof = rooflines(w, st, timed, mean, rbytes, peak_measured)
     if not args.no_probes:  # measured HBM read ceilings at the kernels' own sizes, and at 1 GiB
         for r in (attn_roof, score_roof):
             r["peak_measured"] = hbm_probe(torch, P, r["bytes_per_launch"])
@@ -477,7 +496,8 @@ def bench_layer(cid, args, torch, P, H, W):
     line = base_line(cid, K, args.warmup)
     line.update({
         "value": rbytes / (ms_per_step * 1e-3) / 1e9,
-        "us_per_layer_step": mean["layer"] * 1e3,
+        "us_per_layer_step": timed["layer"] * 1e3,
+        "us_per_layer_step_median": timed["layer_median"] * 1e3,
         "ms_per_step": ms_per_step,
         "config": {"workload": WORKLOADS[cid], "preset": cid, "batch": w.B, "total_blocks": w.total_blocks,
                    "block_size": w.bs, "k_max": w.k_max, "parallelism": "single GPU"},
@@ -506,20 +526,26 @@ def bench_multilayer(args, torch, P, H, W):
     torch.cuda.synchronize()
     K = args.steps
 
-    def run(fn):
+    def run(fn, ev_steps=None):
         for _ in range(args.warmup):
             ml.reset()
-            fn()
+            fn(None)
         torch.cuda.synchronize()
         t = time.perf_counter()
-        for _ in range(K):
+        for k in range(K):
             ml.reset()
-            fn()
+            fn(ev_steps[k] if ev_steps else None)
         torch.cuda.synchronize()
         return (time.perf_counter() - t) / K
 
-    t_overlap = run(ml.run_overlapped)
-    t_chain = run(ml.run_chained)
+    # timing events around the recall copy of every 8th layer inside the timed region (each
+    # record costs a few microseconds on the I/O stream, so not every layer carries them)
+    sampled = list(range(0, len(ml.layers), 8))
+    rec_evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if i in sampled
+                else None for i in range(len(ml.layers))] for _ in range(K)]
+    t_overlap = run(lambda ev: ml.run_overlapped(recall_events=ev), rec_evs)
+    sampled_ms = statistics.mean(sum(step[i][0].elapsed_time(step[i][1]) for i in sampled) for step in rec_evs)
+    t_chain = run(lambda ev: ml.run_chained())
     for st in ml.layers:
         if st.status() != 0:
             raise RuntimeError(f"device status {P.status_string(st.status())}")
@@ -527,15 +553,14 @@ def bench_multilayer(args, torch, P, H, W):
     rbytes = sum(x[2] for x in per_layer)
     blocks = sum(x[0] for x in per_layer)
     runs = sum(x[1] for x in per_layer)
-    # stage timing of every layer inside one chained step
+    # attention time of every layer inside one chained step (untimed)
     evs = [P.EventSet(5) for _ in ml.layers]
     ml.reset()
     for st, e in zip(ml.layers, evs):
         a = st.layer_args()
-        a.events = e.ptr
+        a.events = e.masked_ptr((3, 4))
         P.pulse_decode_layer(a)
     torch.cuda.synchronize()
-    recall_ms = sum(e.elapsed_ms(2, 3) for e in evs)
     attn_ms = sum(e.elapsed_ms(3, 4) for e in evs)
     for e in evs:
         e.destroy()
@@ -550,7 +575,8 @@ def bench_multilayer(args, torch, P, H, W):
     w0 = ml.layers[0].w
     U = w0.unit_bytes
     line = base_line(4, K, args.warmup)
-    recall_GBps = rbytes / (recall_ms * 1e-3) / 1e9
+    sampled_bytes = sum(per_layer[i][2] for i in sampled)
+    recall_GBps = sampled_bytes / (sampled_ms * 1e-3) / 1e9
     line.update({
         "value": rbytes / t_overlap / 1e9,
         "us_per_layer_step": t_overlap * 1e6 / len(ml.layers),
@@ -565,7 +591,8 @@ def bench_multilayer(args, torch, P, H, W):
                          "bytes": hw_units * U // w0.Hkv}},
         "roofline": {"bound": "host_link", "kernel": "recall_copy_kernel", "achieved": recall_GBps,
                      "peak": PCIE5_X16_GBPS, "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS,
-                     "bytes_per_launch": rbytes / len(ml.layers), "traffic": None},
+                     "bytes_per_launch": rbytes / len(ml.layers), "traffic": None,
+                     "timed_layers": sampled},
         "attention_ms_per_step": attn_ms,
         "setup_s": {"generate_and_upload": gen_s},
     })

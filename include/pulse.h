@@ -382,7 +382,9 @@ typedef struct {
     size_t ws_bytes;
     void* const* events;      /* optional host array of 5 hipEvent_t, recorded on the
                                  stream before score, select, recall copy, attention and
-                                 after attention (stage timing); NULL = none */
+                                 after attention (stage timing); NULL = none, and a NULL
+                                 entry is not recorded (each record adds a few
+                                 microseconds to the stream) */
 } pulse_layer_args;
 
 /*

@@ -414,13 +414,15 @@ pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream
     if (st != PULSE_OK || a->B == 0) return st;
     hipStream_t hs = (hipStream_t)stream;
     hipEvent_t* ev = (hipEvent_t*)a->events;
-    if (ev && hipEventRecord(ev[0], hs) != hipSuccess) return PULSE_ERR_HIP;
+    // each record costs a few microseconds on the stream, so absent (NULL) entries are skipped
+    auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], hs) == hipSuccess; };
+    if (!mark(0)) return PULSE_ERR_HIP;
     if (layer_select(*a, hs, ev ? ev[1] : nullptr) != hipSuccess) return PULSE_ERR_HIP;
-    if (ev && hipEventRecord(ev[2], hs) != hipSuccess) return PULSE_ERR_HIP;
+    if (!mark(2)) return PULSE_ERR_HIP;
     if (layer_recall(*a, hs) != hipSuccess) return PULSE_ERR_HIP;
-    if (ev && hipEventRecord(ev[3], hs) != hipSuccess) return PULSE_ERR_HIP;
+    if (!mark(3)) return PULSE_ERR_HIP;
     if (layer_attention(*a, hs) != hipSuccess) return PULSE_ERR_HIP;
-    if (ev && hipEventRecord(ev[4], hs) != hipSuccess) return PULSE_ERR_HIP;
+    if (!mark(4)) return PULSE_ERR_HIP;
     return PULSE_OK;
 }
 

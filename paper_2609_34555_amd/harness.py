@@ -308,7 +308,9 @@ class MultiLayerStep:
         for st in self.layers:
             st.decode_layer(stream=stream)
 
-    def run_overlapped(self):
+    def run_overlapped(self, recall_events=None):
+        """The two-stream step.  recall_events: optional per-layer (start, end) timing events
+        (or None) recorded around that layer's recall copy on the I/O stream."""
         cur = torch.cuda.current_stream()
         io, cmp_ = self.io_stream, self.cmp_stream
         io.wait_stream(cur)
@@ -318,7 +320,12 @@ class MultiLayerStep:
         self.selected[0].record(cmp_)
         for i, st in enumerate(self.layers):
             io.wait_event(self.selected[i])
+            ev = recall_events[i] if recall_events is not None else None
+            if ev is not None:
+                ev[0].record(io)
             st.recall(stream=io)
+            if ev is not None:
+                ev[1].record(io)
             self.recalled[i].record(io)
             if i + 1 < n:  # next layer's selection while this layer's blocks cross the link
                 self.layers[i + 1].select(stream=cmp_)

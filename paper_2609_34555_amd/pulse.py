@@ -465,12 +465,20 @@ class EventSet:
 
     def __init__(self, n: int):
         self.n = n
+        self._masked = []
         self.arr = (ctypes.c_void_p * n)()
         _check(lib().pulse_events_create(n, ctypes.cast(self.arr, ctypes.c_void_p)), "pulse_events_create", True)
 
     @property
     def ptr(self) -> int:
         return ctypes.addressof(self.arr)
+
+    def masked_ptr(self, keep) -> int:
+        """Address of a copy of the handle array in which the entries not in `keep` are
+        NULL (pulse_decode_layer records only the non-NULL ones)."""
+        masked = (ctypes.c_void_p * self.n)(*[self.arr[i] if i in keep else None for i in range(self.n)])
+        self._masked.append(masked)  # kept alive as long as the set
+        return ctypes.addressof(masked)
 
     def elapsed_ms(self, i: int, j: int) -> float:
         ms = ctypes.c_float()
