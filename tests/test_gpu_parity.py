@@ -289,6 +289,35 @@ def test_decode_layer_is_deterministic():
         assert torch.equal(a, b)
 
 
+def test_decode_layer_stage_events_all_some_none():
+    """Stage events change nothing in the results, and NULL entries are skipped: the
+    recorded ones still bracket their stages (recall between events 2 and 3)."""
+    from paper_2609_34555_amd import pulse as P
+
+    spec, s = W.preset(2, ctx_scale=1 / 8)
+    w, st = build(spec, s)
+    outs = []
+    sets = [P.EventSet(5) for _ in range(3)]
+    try:
+        for keep in (None, (0, 1, 2, 3, 4), (2, 3)):
+            a = st.layer_args()
+            if keep is not None:
+                a.events = sets[len(outs)].masked_ptr(keep)
+            st.reset()
+            assert P.pulse_decode_layer(a) == 0
+            torch.cuda.synchronize()
+            assert st.status() == 0
+            outs.append((st.out.clone(), st.lse.clone(), st.table.clone(), st.stats.clone()))
+        for o in outs[1:]:
+            assert all(torch.equal(x, y) for x, y in zip(outs[0], o))
+        for e in sets[1:]:
+            assert e.elapsed_ms(2, 3) > 0.0
+        assert sets[1].elapsed_ms(0, 4) >= sets[1].elapsed_ms(2, 3)
+    finally:
+        for e in sets:
+            e.destroy()
+
+
 def test_decode_layer_config2_full_size():
     """The benchmark's workload (8 x 32K, bf16) at full size, in the same launch
     configuration the benchmark times."""
