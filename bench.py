@@ -314,15 +314,17 @@ def base_line(cid, K, warmup):
             "data": "synthetic (seeded N(0,1) K/V/q, planted heavy blocks; no model weights or datasets)"}
 
 
-def _event_pass(torch, P, st, K, keep):
-    """K steps whose layer-steps record the stage events in `keep` (indices into the five
-    of pulse_layer_args.events; the others are left out).  Returns the EventSets and the
-    host wall time of the K steps."""
-    evs = [P.EventSet(5) for _ in range(K)]
+def _event_pass(torch, P, st, K, keep, every=1):
+    """K steps; every `every`-th layer-step records the stage events in `keep` (indices into
+    the five of pulse_layer_args.events; the others are left out), the rest none.  Returns
+    the EventSets of the recording steps and the host wall time of the K steps."""
+    evs = []
     args = []
-    for e in evs:
+    for k in range(K):
         a = st.layer_args()
-        a.events = e.masked_ptr(keep)
+        if k % every == 0:
+            evs.append(P.EventSet(5))
+            a.events = evs[-1].masked_ptr(keep)
         args.append(a)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -336,7 +338,8 @@ def _event_pass(torch, P, st, K, keep):
 def timed_steps(torch, P, st, K, warmup):
     """W untimed steps, then exactly K timed steps (pulse_decode_layer + pulse_release_recalled),
     bracketed by device synchronisation.  Inside the timed region only the two events around
-    the recall copy (the roofline kernel) are recorded: each record adds ~3 us to the stream.
+    the recall copy (the roofline kernel) are recorded, on every 4th step: each record adds
+    ~3 us to the stream.
     Two untimed passes of K steps follow: events before score and after attention only (the
     chain's duration), then all five (the per-stage split, which carries the records' cost)."""
     plain = st.layer_args()
@@ -346,7 +349,7 @@ def timed_steps(torch, P, st, K, warmup):
     for _ in range(warmup):
         P.pulse_decode_layer(plain)
         st.release(chained=True)
-    evs, wall = _event_pass(torch, P, st, K, (2, 3))  # the timed region
+    evs, wall = _event_pass(torch, P, st, K, (2, 3), every=4)  # the timed region
     recall = [e.elapsed_ms(2, 3) for e in evs]
     chain_evs, _ = _event_pass(torch, P, st, K, (0, 4))
     layer = [e.elapsed_ms(0, 4) for e in chain_evs]
