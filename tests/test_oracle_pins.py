@@ -490,3 +490,70 @@ def test_mam_over_middle_blocks_equals_bruteforce_softmax_mass():
         assert abs(mq[hq] - p[ns * bs:(n - nl) * bs].sum()) < 1e-12
     assert np.allclose(mh, mq.reshape(w.Hkv, w.G).mean(axis=1))
     assert best == int(np.argmax(mh))
+
+
+# ---------------------------------------------------------------- headwise baseline (Sec. 3.4)
+
+def test_missing_counts_hand_worked():
+    """Set difference and runs on a hand-worked table: selected [0, 1, 2, 5, 6, 9] with
+    entries -1 at 1, 2, 5 and 9 -> 4 missing blocks in 3 runs ({1, 2}, {5}, {9});
+    an empty selection and an all-resident one count nothing."""
+    table = np.array([[7, -1, -1, 3, 4, -1, 8, 2, 1, -1],
+                      [0, 1, 2, 3, 4, 5, 6, 7, 8, 9],
+                      [-1] * 10], np.int32)
+    sel = np.full((3, 8), -1, np.int32)
+    sel[0, :6] = [0, 1, 2, 5, 6, 9]
+    sel[1, :4] = [1, 2, 3, 4]
+    cnt = np.array([6, 4, 0], np.int32)
+    units, runs = O.missing_counts(sel, cnt, table)
+    assert list(units) == [4, 0, 0] and list(runs) == [3, 0, 0]
+
+
+def test_missing_counts_agree_with_the_recall_statistics():
+    """The headwise counter and the recall (two separate implementations of Sec. 2.2's set
+    difference) agree on missing blocks and runs for random selections and tables."""
+    rng = np.random.default_rng(12)
+    for trial in range(20):
+        n = rng.integers(1, 40, size=4)
+        blk_off = np.concatenate([[0], np.cumsum(n)]).astype(np.int64)
+        maxb = int(n.max())
+        table = np.full((4, maxb), -1, np.int32)
+        k_max = maxb
+        sel = np.full((4, k_max), -1, np.int32)
+        cnt = np.zeros(4, np.int32)
+        slot = 0
+        for r in range(4):
+            res = np.flatnonzero(rng.random(n[r]) < 0.4)
+            table[r, res] = np.arange(slot, slot + res.size)
+            slot += res.size
+            c = int(rng.integers(0, n[r] + 1))
+            sel[r, :c] = np.sort(rng.choice(n[r], c, replace=False))
+            cnt[r] = c
+        units, runs = O.missing_counts(sel, cnt, table)
+        U = 16
+        n_free = int(units.sum())
+        free = np.arange(slot, slot + n_free, dtype=np.int32)
+        pool = np.zeros((slot + n_free, U), np.uint8)
+        host = np.zeros((int(blk_off[-1]), U), np.uint8)
+        rc, fh, stats = O.recall(host, blk_off, sel, cnt, table.copy(), free, 0, pool, U)
+        assert rc == 0
+        assert stats[0] == units.sum() and stats[1] == runs.sum() and fh == n_free
+
+
+def test_headwise_bs1_each_head_is_its_exact_topk_and_solo_row_is_solohead():
+    """bs = 1: every KV head's headwise selection is the exact top-k of that head's
+    group-mean logits (brute force), and the row of any head equals SoloHead with that head."""
+    w = tiny([90, 33, 5], Hq=8, Hkv=4, d=16, bs=1, seed=41, n_sink=0, n_local=0, k_mid=9)
+    k_mid = np.full(w.B, 9, np.int32)
+    sel, cnt, sc = O.headwise_select(w.kv, w.q, w.blk_off, w.ctx_len, w.Hq, w.Hkv, 1, w.d, O.BF16, k_mid, 0, 0, 12)
+    qf = W.to_float(w.q, "bf16").astype(np.float64)
+    K = W.to_float(k_view(w.kv, w.Hkv, 1, w.d)[:, :, 0, :], "bf16").astype(np.float64)
+    for h in range(w.Hkv):
+        for r in range(w.B):
+            b0, b1 = int(w.blk_off[r]), int(w.blk_off[r + 1])
+            logit = K[b0:b1, h] @ qf[r, h * w.G:(h + 1) * w.G].mean(axis=0)
+            order = np.lexsort((np.arange(b1 - b0), -logit))
+            assert list(sel[h, r, : cnt[h, r]]) == list(np.sort(order[: min(9, b1 - b0)]))
+        dig = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, 1, w.d, O.BF16, h)
+        rc, idx, c1 = O.select(O.score(w.q, dig, w.blk_off, w.Hq, w.Hkv, w.d, O.BF16, h), w.blk_off, k_mid, 0, 0, 12)
+        assert rc == 0 and np.array_equal(idx, sel[h]) and np.array_equal(c1, cnt[h])
