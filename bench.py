@@ -321,7 +321,7 @@ def _event_pass(torch, P, st, K, keep, every=1):
     evs = []
     args = []
     for k in range(K):
-        a = st.layer_args()
+        a = st.layer_args(release_previous=True)
         if k % every == 0:
             evs.append(P.EventSet(5))
             a.events = evs[-1].masked_ptr(keep)
@@ -330,31 +330,29 @@ def _event_pass(torch, P, st, K, keep, every=1):
     t0 = time.perf_counter()
     for a in args:
         P.pulse_decode_layer(a)
-        st.release(chained=True)
     torch.cuda.synchronize()
     return evs, time.perf_counter() - t0
 
 
 def timed_steps(torch, P, st, K, warmup):
-    """W untimed steps, then exactly K timed steps (pulse_decode_layer + pulse_release_recalled),
-    bracketed by device synchronisation.  Inside the timed region only the two events around
+    """W untimed steps, then exactly K timed steps, bracketed by device synchronisation.  A
+    step is pulse_decode_layer with release_previous set: it first undoes the previous step's
+    recall (inside the scoring kernel; the hot set stays fixed-size), so every step recalls
+    the same blocks.  Inside the timed region only the two events around
     the recall copy (the roofline kernel) are recorded, on every 4th step: each record adds
     ~3 us to the stream.
     Two untimed passes of K steps follow: events before score and after attention only (the
     chain's duration), then all five (the per-stage split, which carries the records' cost)."""
-    plain = st.layer_args()
-    # a step = the layer-step plus the step-end release of its recall (the hot set stays
-    # fixed-size), so every step recalls the same blocks; state is reset once, untimed
-    st.reset()
+    step = st.layer_args(release_previous=True)
+    st.reset()  # once, untimed: nothing recalled yet
     for _ in range(warmup):
-        P.pulse_decode_layer(plain)
-        st.release(chained=True)
+        P.pulse_decode_layer(step)
     evs, wall = _event_pass(torch, P, st, K, (2, 3), every=4)  # the timed region
     recall = [e.elapsed_ms(2, 3) for e in evs]
     chain_evs, _ = _event_pass(torch, P, st, K, (0, 4))
     layer = [e.elapsed_ms(0, 4) for e in chain_evs]
     stage_evs, _ = _event_pass(torch, P, st, K, (0, 1, 2, 3, 4))
-    P.pulse_decode_layer(plain)  # untimed: leaves this step's recall statistics and tables in place
+    P.pulse_decode_layer(step)  # untimed: leaves this step's recall statistics and tables in place
     torch.cuda.synchronize()
     stage = {"score": [], "select": [], "recall": [], "attention": [], "layer": []}
     for e in stage_evs:
@@ -530,13 +528,14 @@ def bench_multilayer(args, torch, P, H, W):
     K = args.steps
 
     def run(fn, ev_steps=None):
+        # every step ends with (or starts by) releasing each layer's recall, so every step
+        # recalls the same blocks; the tables are restored once, untimed
+        ml.reset()
         for _ in range(args.warmup):
-            ml.reset()
             fn(None)
         torch.cuda.synchronize()
         t = time.perf_counter()
         for k in range(K):
-            ml.reset()
             fn(ev_steps[k] if ev_steps else None)
         torch.cuda.synchronize()
         return (time.perf_counter() - t) / K
@@ -546,9 +545,9 @@ def bench_multilayer(args, torch, P, H, W):
     sampled = list(range(0, len(ml.layers), 8))
     rec_evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) if i in sampled
                 else None for i in range(len(ml.layers))] for _ in range(K)]
-    t_overlap = run(lambda ev: ml.run_overlapped(recall_events=ev), rec_evs)
+    t_overlap = run(lambda ev: ml.run_overlapped(recall_events=ev, release=True), rec_evs)
     sampled_ms = statistics.mean(sum(step[i][0].elapsed_time(step[i][1]) for i in sampled) for step in rec_evs)
-    t_chain = run(lambda ev: ml.run_chained())
+    t_chain = run(lambda ev: ml.run_chained(release_previous=True))
     for st in ml.layers:
         if st.status() != 0:
             raise RuntimeError(f"device status {P.status_string(st.status())}")

@@ -385,6 +385,16 @@ typedef struct {
                                  after attention (stage timing); NULL = none, and a NULL
                                  entry is not recorded (each record adds a few
                                  microseconds to the stream) */
+    int32_t release_previous; /* nonzero: before selecting, undo the recall of the
+                                 previous pulse_decode_layer made with these buffers
+                                 (table entries back to -1, free_head rewound; the hot
+                                 set stays fixed-size, Sec. 4.2), inside the scoring
+                                 kernel instead of a launch of its own.  Only a recall
+                                 that moved bytes (stats->bytes > 0) is undone; the
+                                 statistics are left for this step's recall to
+                                 overwrite.  A recall made by pulse_recall_gather or
+                                 the engine is released with pulse_release_recalled.
+                                 0: no release */
 } pulse_layer_args;
 
 /*

@@ -358,8 +358,11 @@ namespace pulse {
 // and select.
 hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mid) {
     const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
+    const ReleaseArgs rel{at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt), a.B, a.k_max,
+                          a.block_table, a.max_blocks, a.free_head, a.stats, a.dev_status};
     hipError_t e = launch_score(a.shape, a.q, a.digests, a.blk_off, a.B, a.total_blocks, a.solo_kv_head,
-                                a.n_sink_blocks, a.n_local_blocks, at<float>(a.ws, w.scores), 1, hs);
+                                a.n_sink_blocks, a.n_local_blocks, at<float>(a.ws, w.scores), 1, hs,
+                                a.release_previous ? &rel : nullptr);
     if (e != hipSuccess) return e;
     if (mid && (e = hipEventRecord(mid, hs)) != hipSuccess) return e;
     return launch_select(a.blk_off, a.B, a.total_blocks, at<float>(a.ws, w.scores), a.k_mid, a.n_sink_blocks,

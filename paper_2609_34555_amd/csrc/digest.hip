@@ -127,7 +127,8 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
                                                     const uint16_t* __restrict__ digests,
                                                     const int64_t* __restrict__ blk_off, int32_t B,
                                                     int64_t total_blocks, int32_t Hq, int32_t solo,
-                                                    int32_t n_sink, int32_t n_local, float* __restrict__ scores) {
+                                                    int32_t n_sink, int32_t n_local, float* __restrict__ scores,
+                                                    ReleaseArgs rel, int32_t do_release) {
     extern __shared__ int64_t s_off[];
     const int head = gridDim.y > 1 ? (int)blockIdx.y : solo;
     digests += (size_t)blockIdx.y * total_blocks * 2 * kHeadDim;
@@ -147,6 +148,9 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
             dmx[it] = score_load<NT>(dg + 16 + sub);
         }
     }
+    // the previous step's release, on the side (independent of the scores)
+    if (do_release && blockIdx.y == 0)
+        release_entries(rel, (int64_t)blockIdx.x * 256 + threadIdx.x, (int64_t)gridDim.x * 256, true);
     for (int i = threadIdx.x; i <= B; i += 256) s_off[i] = blk_off[i];
     __syncthreads();
     int cur_r = -1;
@@ -203,25 +207,28 @@ hipError_t launch_build_digests(const pulse_shape& s, const void* kv, const int6
 template <int DT, int G>
 static void launch_score_t(int32_t heads, hipStream_t st, const void* q, const void* digests, const int64_t* blk_off,
                            int32_t B, int64_t total, int32_t Hq, int32_t solo, int32_t n_sink, int32_t n_local,
-                           float* scores) {
+                           float* scores, const ReleaseArgs* rel) {
     const size_t lds = sizeof(int64_t) * ((size_t)B + 1);
+    const ReleaseArgs ra = rel ? *rel : ReleaseArgs{};
+    const int32_t dr = rel != nullptr;
     if (total * heads > kScoreLargeBlocks) {
         const dim3 grid((unsigned)((total + 31) / 32), (unsigned)heads);
         hipLaunchKernelGGL((score_kernel<DT, G, 2, true>), grid, dim3(256), lds, st, (const uint16_t*)q,
-                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores);
+                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, ra, dr);
     } else {
         const dim3 grid((unsigned)((total + 15) / 16), (unsigned)heads);
         hipLaunchKernelGGL((score_kernel<DT, G, 1, false>), grid, dim3(256), lds, st, (const uint16_t*)q,
-                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores);
+                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, ra, dr);
     }
 }
 
 template <int DT>
 static void launch_score_dt(int G, int32_t heads, hipStream_t st, const void* q, const void* digests,
                             const int64_t* blk_off, int32_t B, int64_t total, int32_t Hq, int32_t solo,
-                            int32_t n_sink, int32_t n_local, float* scores) {
+                            int32_t n_sink, int32_t n_local, float* scores, const ReleaseArgs* rel) {
 #define PULSE_SCORE_CASE(g) \
-    case g: launch_score_t<DT, g>(heads, st, q, digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores); break;
+    case g: launch_score_t<DT, g>(heads, st, q, digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, rel); \
+        break;
     switch (G) {
         PULSE_SCORE_CASE(1) PULSE_SCORE_CASE(2) PULSE_SCORE_CASE(3) PULSE_SCORE_CASE(4)
         PULSE_SCORE_CASE(5) PULSE_SCORE_CASE(6) PULSE_SCORE_CASE(7) PULSE_SCORE_CASE(8)
@@ -234,15 +241,15 @@ static void launch_score_dt(int G, int32_t heads, hipStream_t st, const void* q,
 
 hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
                         int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
-                        float* scores, int32_t heads, hipStream_t st) {
-    if (total_blocks == 0) return hipSuccess;
+                        float* scores, int32_t heads, hipStream_t st, const ReleaseArgs* rel) {
+    if (total_blocks == 0) return hipSuccess;  // no blocks: no recall to release either
     const int G = s.num_q_heads / s.num_kv_heads;
     if (s.dtype == PULSE_BF16)
         launch_score_dt<PULSE_BF16>(G, heads, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
-                                    n_local, scores);
+                                    n_local, scores, rel);
     else
         launch_score_dt<PULSE_F16>(G, heads, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
-                                   n_local, scores);
+                                   n_local, scores, rel);
     return hipGetLastError();
 }
 

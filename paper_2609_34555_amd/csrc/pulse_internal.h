@@ -94,9 +94,59 @@ hipError_t launch_build_digests(const pulse_shape& s, const void* kv, const int6
 
 // heads == 1: score with KV head `solo`; heads == Hkv: every head h scores with
 // its own digests (digests and scores stacked along h).
+// The step-end release of the previous recall (see launch_release), when the
+// scoring kernel performs it on the side.
+struct ReleaseArgs {
+    const int32_t* miss_list;
+    const int32_t* miss_cnt;
+    int32_t B, k_max;
+    int32_t* table;
+    int32_t max_blocks;
+    int32_t* free_head;
+    pulse_recall_stats* stats;
+    int32_t* status;
+};
+// Release work of thread `e0` of `stride` (grid-stride over the B * k_max plan
+// entries): an entry's table slot returns to -1; thread 0 alone moves the
+// free-list head back.  Standalone (fused = false): the table pass runs
+// unconditionally (-1 is right whether or not the recall moved the block) and
+// thread 0 clears the statistics, so a second release changes nothing.  Fused
+// into the next layer-step's scoring kernel: only a recall that moved bytes is
+// undone, every thread reads that from the statistics, and none clears them
+// (the recall of the same step overwrites them), so no thread reads what
+// another writes.
+__device__ inline void release_entries(const ReleaseArgs& a, int64_t e0, int64_t stride, bool fused) {
+    if (fused && a.stats->bytes <= 0) return;
+    for (int64_t e = e0; e < (int64_t)a.B * a.k_max; e += stride) {
+        const int32_t r = (int32_t)(e / a.k_max), i = (int32_t)(e % a.k_max);
+        const int32_t n = a.miss_cnt[r];
+        if (n < 0 || n > a.k_max) {
+            if (i == 0) report(a.status, PULSE_ERR_BAD_INDEX);
+        } else if (i < n) {
+            const int32_t j = a.miss_list[(size_t)r * a.k_max + i];
+            if (j >= 0 && j < a.max_blocks) a.table[(size_t)r * a.max_blocks + j] = -1;
+            else report(a.status, PULSE_ERR_BAD_INDEX);
+        }
+    }
+    if (e0 == 0 && a.stats->bytes > 0) {
+        if (*a.free_head < a.stats->n_missing) {
+            report(a.status, PULSE_ERR_BAD_INDEX);
+        } else {
+            *a.free_head -= a.stats->n_missing;
+            if (!fused) {
+                a.stats->n_missing = 0;
+                a.stats->n_runs = 0;
+                a.stats->bytes = 0;
+            }
+        }
+    }
+}
+// rel != nullptr: the scoring kernel also releases the recall described by rel
+// (every entry's table reset, then the free-list head and statistics), which
+// the kernel boundary orders before the selection that follows.
 hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
                         int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
-                        float* scores, int32_t heads, hipStream_t st);
+                        float* scores, int32_t heads, hipStream_t st, const ReleaseArgs* rel = nullptr);
 
 // select (a3); when table != nullptr the set difference (a4) is folded in and
 // the recall plan (miss list, counts, runs, free_head snapshot) is written.

@@ -232,32 +232,9 @@ __global__ __launch_bounds__(kCopyThreads) void probe_copy_kernel(const uint8_t*
 // reads and clears them and moves the free-list head back.
 constexpr int kReleaseThreads = 256;
 
-__global__ __launch_bounds__(kReleaseThreads) void release_kernel(
-    const int32_t* __restrict__ miss_list, const int32_t* __restrict__ miss_cnt, int32_t B, int32_t k_max,
-    int32_t* __restrict__ table, int32_t max_blocks, int32_t* __restrict__ free_head,
-    pulse_recall_stats* __restrict__ stats, int32_t* status) {
-    const int64_t e = (int64_t)blockIdx.x * kReleaseThreads + threadIdx.x;
-    if (e < (int64_t)B * k_max) {
-        const int32_t r = (int32_t)(e / k_max), i = (int32_t)(e % k_max);
-        const int32_t n = miss_cnt[r];
-        if (n < 0 || n > k_max) {
-            if (i == 0) report(status, PULSE_ERR_BAD_INDEX);
-        } else if (i < n) {
-            const int32_t j = miss_list[(size_t)r * k_max + i];
-            if (j >= 0 && j < max_blocks) table[(size_t)r * max_blocks + j] = -1;
-            else report(status, PULSE_ERR_BAD_INDEX);
-        }
-    }
-    if (e == 0 && stats->bytes > 0) {
-        if (*free_head < stats->n_missing) {
-            report(status, PULSE_ERR_BAD_INDEX);
-        } else {
-            *free_head -= stats->n_missing;
-            stats->n_missing = 0;
-            stats->n_runs = 0;
-            stats->bytes = 0;
-        }
-    }
+__global__ __launch_bounds__(kReleaseThreads) void release_kernel(ReleaseArgs a) {
+    release_entries(a, (int64_t)blockIdx.x * kReleaseThreads + threadIdx.x, (int64_t)gridDim.x * kReleaseThreads,
+                    false);
 }
 
 hipError_t launch_release(const int32_t* miss_list, const int32_t* miss_cnt, int32_t B, int32_t k_max,
@@ -265,9 +242,9 @@ hipError_t launch_release(const int32_t* miss_list, const int32_t* miss_cnt, int
                           int32_t* status, hipStream_t st) {
     if (B == 0) return hipSuccess;
     const int64_t n = (int64_t)B * k_max;
+    const ReleaseArgs a{miss_list, miss_cnt, B, k_max, table, max_blocks, free_head, stats, status};
     hipLaunchKernelGGL(release_kernel, dim3((unsigned)((n + kReleaseThreads - 1) / kReleaseThreads)),
-                       dim3(kReleaseThreads), 0, st, miss_list, miss_cnt, B, k_max, table, max_blocks, free_head,
-                       stats, status);
+                       dim3(kReleaseThreads), 0, st, a);
     return hipGetLastError();
 }
 

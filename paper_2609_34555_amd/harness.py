@@ -114,12 +114,15 @@ class LayerState:
         return dst
 
     def reset(self):
-        """Restore the block table and free-list head of the step's start; clear status."""
+        """Restore the block table and free-list head of the step's start; clear status and
+        the recall statistics (no recall is left to release)."""
         self.table.copy_(self.table0)
         self.free_head.copy_(self.free_head0)
         self.dev_status.zero_()
+        self.stats.zero_()
 
-    def layer_args(self, digests: Optional[torch.Tensor] = None) -> P.pulse_layer_args:
+    def layer_args(self, digests: Optional[torch.Tensor] = None, release_previous: bool = False
+                   ) -> P.pulse_layer_args:
         w = self.w
         a = P.pulse_layer_args()
         a.shape = self.shape
@@ -151,10 +154,13 @@ class LayerState:
         a.dev_status = self.dev_status.data_ptr()
         a.ws = self.ws.data_ptr()
         a.ws_bytes = self.ws_bytes
+        a.release_previous = 1 if release_previous else 0
         return a
 
-    def decode_layer(self, stream=None):
-        P.pulse_decode_layer(self.layer_args(), stream=stream)
+    def decode_layer(self, stream=None, release_previous=False):
+        """pulse_decode_layer; release_previous: first undo the previous layer-step's recall
+        (in the scoring kernel) instead of a separate release()."""
+        P.pulse_decode_layer(self.layer_args(release_previous=release_previous), stream=stream)
 
     def release(self, chained=True, stream=None):
         """Step-end release of the last recall (pulse_release_recalled): table and free
@@ -304,13 +310,17 @@ class MultiLayerStep:
         for st in self.layers:
             st.reset()
 
-    def run_chained(self, stream=None):
+    def run_chained(self, stream=None, release_previous=False):
+        """One pulse_decode_layer per layer on one stream; release_previous: each layer first
+        undoes its previous step's recall (the hot set stays fixed-size)."""
         for st in self.layers:
-            st.decode_layer(stream=stream)
+            st.decode_layer(stream=stream, release_previous=release_previous)
 
-    def run_overlapped(self, recall_events=None):
+    def run_overlapped(self, recall_events=None, release=False):
         """The two-stream step.  recall_events: optional per-layer (start, end) timing events
-        (or None) recorded around that layer's recall copy on the I/O stream."""
+        (or None) recorded around that layer's recall copy on the I/O stream.  release: after
+        each layer's attention, release its recall on the compute stream (the step-end
+        release; it overlaps the next recalls)."""
         cur = torch.cuda.current_stream()
         io, cmp_ = self.io_stream, self.cmp_stream
         io.wait_stream(cur)
@@ -332,6 +342,8 @@ class MultiLayerStep:
                 self.selected[i + 1].record(cmp_)
             cmp_.wait_event(self.recalled[i])
             st.attention(stream=cmp_)
+            if release:
+                st.release(chained=False, stream=cmp_)
         cur.wait_stream(io)
         cur.wait_stream(cmp_)
 

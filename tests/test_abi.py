@@ -5,6 +5,8 @@ import os
 import re
 import subprocess
 
+import pytest
+
 from paper_2609_34555_amd import pulse as P
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -147,3 +149,40 @@ def test_oracle_and_product_share_nothing():
             txt = open(os.path.join(ROOT, "oracle", f)).read()
             assert "paper_2609_34555_amd" not in re.findall(r"(?:import|from)\s+([\w.]+)", txt), f
             assert "#include" not in txt or ("pulse_internal" not in txt and "pulse.h\"" not in txt), f
+
+
+def test_binding_structs_match_the_header_layout(tmp_path):
+    """Every struct the binding passes by pointer has the header's size and field offsets
+    (compiled from include/pulse.h with the host C compiler)."""
+    import ctypes
+    import shutil
+    import subprocess
+
+    from paper_2609_34555_amd import pulse as P
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    structs = [P.pulse_shape, P.pulse_recall_stats, P.pulse_ioaa_params, P.pulse_layer_args,
+               P.pulse_normal_layer, P.pulse_irq_stats]
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "pulse.h"', "int main(void) {"]
+    for cls in structs:
+        name = cls.__name__
+        lines.append(f'printf("{name} size %zu\\n", sizeof({name}));')
+        for f, _ in cls._fields_:
+            lines.append(f'printf("{name} {f} %zu\\n", offsetof({name}, {f}));')
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    inc = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include")
+    subprocess.run([cc, "-std=c99", "-I", inc, str(src), "-o", str(exe)], check=True, capture_output=True)
+    got = {}
+    for line in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.splitlines():
+        name, field, value = line.split()
+        got[(name, field)] = int(value)
+    for cls in structs:
+        name = cls.__name__
+        assert got[(name, "size")] == ctypes.sizeof(cls), name
+        for f, _ in cls._fields_:
+            assert got[(name, f)] == getattr(cls, f).offset, (name, f)
