@@ -119,6 +119,16 @@ def test_chained_layer_at_maximum_batch():
     w, st = build(spec, s)
     res = full_check(w, st, chained=True)
     say(f"  {w.B} requests, {res['stats'][0]} recalled blocks, attn max err {res['attn_err']}")
+    # the next step with the fused release (B * k_max plan entries spread over the scoring
+    # grid) repeats the step exactly
+    table1, fh1, stats1 = st.table.clone(), int(st.free_head.item()), st.recall_stats()
+    out1 = st.out.clone()
+    st.out.zero_()
+    st.decode_layer(release_previous=True)
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    assert torch.equal(st.table, table1) and int(st.free_head.item()) == fh1 and st.recall_stats() == stats1
+    assert torch.equal(st.out, out1)
 
 
 def test_select_duplicate_blocks_take_lowest_index():
