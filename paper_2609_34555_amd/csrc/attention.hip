@@ -121,10 +121,10 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
     const size_t v_head = (size_t)Hkv * BS * kHeadDim + (size_t)h * kHeadDim * BS;
     const int tokens = ne * BS;
 
-    // K/V operand loads of one 32-token step starting at sequence token t0
+    // K and V operand loads of one 32-token step starting at sequence token t0
     // K: MFMA row m = col maps to token 8*(col/4) + 4*sub + col%4;
     // V: lane group grp holds tokens 8*grp .. 8*grp+7 of channel col + 16*tile.
-    auto load_step = [&](int t0, vec (&ka)[2][4], vec (&vb)[8]) {
+    auto load_k = [&](int t0, vec (&ka)[2][4]) {
         const int ka_seq = t0 + 8 * (col >> 2);
         const int ka_e = ka_seq / BS;
         const int ka_slot = __shfl(my_slot, ka_e < ne ? ka_e : 0);
@@ -137,6 +137,8 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
 #pragma unroll
             for (int kc = 0; kc < 4; ++kc) ka[sub][kc] = ok ? load_vec<DT>(kp + 32 * kc) : zero_vec<DT>();
         }
+    };
+    auto load_v = [&](int t0, vec (&vb)[8]) {
         const int pv_seq = t0 + 8 * grp;
         const int pv_e = pv_seq / BS;
         const int pv_slot = __shfl(my_slot, pv_e < ne ? pv_e : 0);
@@ -146,13 +148,15 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
         for (int t = 0; t < 8; ++t) vb[t] = pv_ok ? load_vec<DT>(vp + (size_t)16 * t * BS) : zero_vec<DT>();
     };
 
-    // One 32-token step at a time.  The other resident waves of the SIMD hide the load
-    // latency; prefetching the next step into registers (measured) was 1-2% slower,
-    // at 223 instead of 154 VGPRs.
+    // One 32-token step at a time: K is loaded first, V once the S tile is issued, so
+    // the V loads overlap the softmax and fewer operands are live (143 VGPRs, 3 waves
+    // per SIMD).  The other resident waves hide the load latency.  Measured slower:
+    // loading K and V together (154 VGPRs; 2-5%), and prefetching the next step into
+    // registers as well (223 VGPRs; another 1-2%).
 #pragma unroll 1
     for (int t0 = 0; t0 < tokens; t0 += kChunkTokens) {
         vec ka[2][4], vb[8];
-        load_step(t0, ka, vb);
+        load_k(t0, ka);
         const int pv_seq = t0 + 8 * grp;
         const int pv_e = pv_seq / BS;
         const int pv_slot = __shfl(my_slot, pv_e < ne ? pv_e : 0);
@@ -166,6 +170,7 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
             s1 = M::mac(ka[0][kc], qb[kc], s1);
             s2 = M::mac(ka[1][kc], qb[kc], s2);
         }
+        load_v(t0, vb);
         // lane (col, grp) now holds query col, tokens pv_seq + 0..7
         float x[8];
 #pragma unroll
