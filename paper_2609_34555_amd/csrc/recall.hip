@@ -139,9 +139,9 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     const int32_t* __restrict__ run_cnt, const int32_t* __restrict__ req_err, const int32_t* __restrict__ misc,
     pulse_recall_stats* __restrict__ stats, int32_t* status, int32_t copy_xcds) {
     __shared__ int32_t off[kMaxBatch + 1];
-    __shared__ uint32_t part_sum[kCopyThreads];
+    __shared__ uint32_t wave_tot[kCopyThreads / kWave];
     __shared__ uint32_t sh_runs, sh_bad;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     // exclusive scan of miss_cnt: thread t owns a contiguous segment
     const int per = (B + kCopyThreads - 1) / kCopyThreads;
     const int s0 = tid * per, s1 = min(B, s0 + per);
@@ -151,13 +151,18 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
         racc += (uint32_t)run_cnt[i];
         bad |= (uint32_t)(req_err[i] != 0);
     }
-    part_sum[tid] = acc;
+    uint32_t incl = acc;  // inclusive scan within the wave, then wave totals through LDS
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = (uint32_t)__shfl_up((int)incl, o);
+        if (lane >= o) incl += y;
+    }
+    if (lane == kWave - 1) wave_tot[wave] = incl;
     if (tid == 0) { sh_runs = 0; sh_bad = 0; }
     __syncthreads();
     if (racc) atomicAdd(&sh_runs, racc);
     if (bad) atomicOr(&sh_bad, 1u);
-    uint32_t before = 0;
-    for (int t = 0; t < tid; ++t) before += part_sum[t];
+    uint32_t before = incl - acc;
+    for (int w = 0; w < wave; ++w) before += wave_tot[w];
     for (int i = s0; i < s1; ++i) {
         off[i] = (int32_t)before;
         before += (uint32_t)miss_cnt[i];
