@@ -188,7 +188,8 @@ PULSE_API pulse_status pulse_select_headwise(const pulse_shape* shape, const voi
  * gather-scatter engine: 0).  A recall that moved no bytes (exhaustion, an
  * error, nothing missing) leaves nothing to undo; a second release is a no-op.
  * Stream-ordered, no host sync; inconsistent plans report BAD_INDEX in
- * dev_status.
+ * dev_status.  pulse_decode_layer can instead release its predecessor's
+ * recall itself (pulse_layer_args.release_previous).
  */
 PULSE_API pulse_status pulse_release_recalled(const pulse_shape* shape, int32_t B, int32_t k_max,
                                               int64_t total_blocks, int32_t* block_table, int32_t max_blocks,
