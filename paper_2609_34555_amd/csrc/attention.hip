@@ -151,8 +151,10 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
     // One 32-token step at a time: K is loaded first, V once the S tile is issued, so
     // the V loads overlap the softmax and fewer operands are live (143 VGPRs, 3 waves
     // per SIMD).  The other resident waves hide the load latency.  Measured slower:
-    // loading K and V together (154 VGPRs; 2-5%), and prefetching the next step into
-    // registers as well (223 VGPRs; another 1-2%).
+    // loading K and V together (154 VGPRs; 2-5%), prefetching the next step into
+    // registers as well (223 VGPRs; another 1-2%), and, for splits of two steps,
+    // issuing all four loads before the first product (177 VGPRs; 11% slower on
+    // 8 requests x 2048 selected tokens).
 #pragma unroll 1
     for (int t0 = 0; t0 < tokens; t0 += kChunkTokens) {
         vec ka[2][4], vb[8];

@@ -148,33 +148,45 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
             dmx[it] = score_load<NT>(dg + 16 + sub);
         }
     }
+    // Up to G = 6, the query rows of the request that holds the first block if
+    // every request had the same length (exact for equal contexts) are loaded
+    // with the digests, and a wrong guess is reloaded once the offsets are
+    // known.  Larger groups load them then: holding G x 4 more registers across
+    // the barrier would take the kernel past 64 VGPRs (8 waves per SIMD).
+    constexpr bool kEarlyQ = G <= 6;
+    uint32_t qp[G][4];
+    auto load_q = [&](int rq) {
+        const uint16_t* qr = q + ((size_t)rq * Hq + (size_t)head * G) * kHeadDim + c8;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const u32x4 v = *reinterpret_cast<const u32x4*>(qr + (size_t)g * kHeadDim);
+#pragma unroll
+            for (int p = 0; p < 4; ++p) qp[g][p] = v[p];
+        }
+    };
+    int q_r = -1;
+    if constexpr (kEarlyQ) {
+        q_r = base < total_blocks ? (int)(base * B / total_blocks) : 0;
+        q_r = q_r < B ? q_r : B - 1;
+        load_q(q_r);
+    }
     // the previous step's release, on the side (independent of the scores)
     if (do_release && blockIdx.y == 0)
         release_entries(rel, (int64_t)blockIdx.x * 256 + threadIdx.x, (int64_t)gridDim.x * 256, true);
     for (int i = threadIdx.x; i <= B; i += 256) s_off[i] = blk_off[i];
     __syncthreads();
-    int cur_r = -1;
     int64_t r_lo = 0, r_hi = 0;
-    uint32_t qp[G][4], qm[G][4];
 #pragma unroll
     for (int it = 0; it < ITERS; ++it) {
         const int64_t b = base + 16 * it;
         if (b >= total_blocks) break;
         if (b >= r_hi || b < r_lo) {
-            cur_r = find_request_lds(s_off, B, b);
+            const int cur_r = find_request_lds(s_off, B, b);
             r_lo = s_off[cur_r];
             r_hi = s_off[cur_r + 1];
-            const uint16_t* qr = q + ((size_t)cur_r * Hq + (size_t)head * G) * kHeadDim + c8;
-#pragma unroll
-            for (int g = 0; g < G; ++g) {
-                u32x4 v = *reinterpret_cast<const u32x4*>(qr + (size_t)g * kHeadDim);
-#pragma unroll
-                for (int p = 0; p < 4; ++p) {
-                    qp[g][p] = v[p];
-                    // 0xFFFF in each half whose q is non-negative (sign bit clear)
-                    const uint32_t sgn = v[p] & 0x80008000u;
-                    qm[g][p] = ~((sgn >> 15) * 0xFFFFu);
-                }
+            if (cur_r != q_r) {
+                load_q(cur_r);
+                q_r = cur_r;
             }
         }
         const int64_t j = b - r_lo;
@@ -185,7 +197,10 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t* __restrict__
         for (int g = 0; g < G; ++g)
 #pragma unroll
             for (int p = 0; p < 4; ++p) {
-                const uint32_t sel = (dmx[it][p] & qm[g][p]) | (dmn[it][p] & ~qm[g][p]);
+                // 0xFFFF in each half whose q is non-negative (sign bit clear), formed
+                // here rather than kept: G x 4 fewer live registers
+                const uint32_t qm = ~(((qp[g][p] & 0x80008000u) >> 15) * 0xFFFFu);
+                const uint32_t sel = (dmx[it][p] & qm) | (dmn[it][p] & ~qm);
                 acc = dot2<DT>(qp[g][p], sel, acc);
             }
 #pragma unroll

@@ -115,24 +115,44 @@ struct ReleaseArgs {
 // undone, every thread reads that from the statistics, and none clears them
 // (the recall of the same step overwrites them), so no thread reads what
 // another writes.
+//
+// The loads of a thread's first entry (its request's miss count and its list
+// value), the statistics and the free-list head do not depend on one another,
+// so all of them are issued before any is used: one memory round trip instead
+// of a chain of three.  A list value past the request's count is read but not
+// used (the list spans B * k_max entries).
 __device__ inline void release_entries(const ReleaseArgs& a, int64_t e0, int64_t stride, bool fused) {
-    if (fused && a.stats->bytes <= 0) return;
-    for (int64_t e = e0; e < (int64_t)a.B * a.k_max; e += stride) {
+    const int64_t n_ent = (int64_t)a.B * a.k_max;
+    const bool head = e0 == 0;
+    int32_t n_missing = 0, fh = 0;
+    int64_t bytes = 0;
+    if (fused || head) {
+        n_missing = a.stats->n_missing;
+        bytes = a.stats->bytes;
+    }
+    if (head) fh = *a.free_head;
+    int32_t n_first = 0, j_first = -1;
+    if (e0 < n_ent) {
+        n_first = a.miss_cnt[e0 / a.k_max];
+        j_first = a.miss_list[e0];
+    }
+    if (fused && bytes <= 0) return;
+    for (int64_t e = e0; e < n_ent; e += stride) {
         const int32_t r = (int32_t)(e / a.k_max), i = (int32_t)(e % a.k_max);
-        const int32_t n = a.miss_cnt[r];
+        const int32_t n = e == e0 ? n_first : a.miss_cnt[r];
         if (n < 0 || n > a.k_max) {
             if (i == 0) report(a.status, PULSE_ERR_BAD_INDEX);
         } else if (i < n) {
-            const int32_t j = a.miss_list[(size_t)r * a.k_max + i];
+            const int32_t j = e == e0 ? j_first : a.miss_list[e];
             if (j >= 0 && j < a.max_blocks) a.table[(size_t)r * a.max_blocks + j] = -1;
             else report(a.status, PULSE_ERR_BAD_INDEX);
         }
     }
-    if (e0 == 0 && a.stats->bytes > 0) {
-        if (*a.free_head < a.stats->n_missing) {
+    if (head && bytes > 0) {
+        if (fh < n_missing) {
             report(a.status, PULSE_ERR_BAD_INDEX);
         } else {
-            *a.free_head -= a.stats->n_missing;
+            *a.free_head = fh - n_missing;
             if (!fused) {
                 a.stats->n_missing = 0;
                 a.stats->n_runs = 0;
