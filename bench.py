@@ -82,15 +82,19 @@ def link_probes(torch, P, st, holder):
     import numpy as np
 
     sweep = {}
-    for unit in (8 << 10, 64 << 10, 1 << 20):
+    for unit in (8 << 10, 16 << 10, 32 << 10, 64 << 10, 128 << 10, 256 << 10, 512 << 10, 1 << 20):
         n = min(512, nb // unit)
         src = np.random.default_rng(0).permutation(nb // unit)[:n].astype(np.int64)
         dst = np.arange(n, dtype=np.int64)
-        e0.record()
-        P.pulse_baseline_memcpy_units(holder[0].ptr, dev, src, dst, n, unit)
-        e1.record()
-        torch.cuda.synchronize()
-        sweep[f"{unit >> 10}KiB"] = n * unit / (e0.elapsed_time(e1) * 1e-3) / 1e9
+        times = []
+        for rep in range(4):  # one warm-up, then the median of three
+            e0.record()
+            P.pulse_baseline_memcpy_units(holder[0].ptr, dev, src, dst, n, unit)
+            e1.record()
+            torch.cuda.synchronize()
+            if rep:
+                times.append(e0.elapsed_time(e1))
+        sweep[f"{unit >> 10}KiB"] = n * unit / (statistics.median(times) * 1e-3) / 1e9
     res["memcpy_per_unit_GBps"] = sweep
     del dev, host
     return res
@@ -314,17 +318,21 @@ def base_line(cid, K, warmup):
             "data": "synthetic (seeded N(0,1) K/V/q, planted heavy blocks; no model weights or datasets)"}
 
 
-def _event_pass(torch, P, st, K, keep, every=1):
+def _event_pass(torch, P, st, K, keep, every=1, split=False):
     """K steps; every `every`-th layer-step records the stage events in `keep` (indices into
-    the five of pulse_layer_args.events; the others are left out), the rest none.  Returns
-    the EventSets of the recording steps and the host wall time of the K steps."""
+    the five of pulse_layer_args.events; the others are left out), the rest none; with
+    `split`, event 5 is recorded between the split-K attention kernel and its combine
+    (pulse_layer_args.attn_split_event).  Returns the EventSets of the recording steps and
+    the host wall time of the K steps."""
     evs = []
     args = []
     for k in range(K):
         a = st.layer_args(release_previous=True)
         if k % every == 0:
-            evs.append(P.EventSet(5))
+            evs.append(P.EventSet(6))
             a.events = evs[-1].masked_ptr(keep)
+            if split:
+                a.attn_split_event = evs[-1].arr[5]
         args.append(a)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -342,7 +350,8 @@ def timed_steps(torch, P, st, K, warmup):
     the recall copy (the roofline kernel) are recorded, on every 4th step: each record adds
     ~3 us to the stream.
     Two untimed passes of K steps follow: events before score and after attention only (the
-    chain's duration), then all five (the per-stage split, which carries the records' cost)."""
+    chain's duration), then all five plus the one between the split-K attention kernel and
+    its combine (the per-stage split, which carries the records' cost)."""
     step = st.layer_args(release_previous=True)
     st.reset()  # once, untimed: nothing recalled yet
     for _ in range(warmup):
@@ -351,15 +360,18 @@ def timed_steps(torch, P, st, K, warmup):
     recall = [e.elapsed_ms(2, 3) for e in evs]
     chain_evs, _ = _event_pass(torch, P, st, K, (0, 4))
     layer = [e.elapsed_ms(0, 4) for e in chain_evs]
-    stage_evs, _ = _event_pass(torch, P, st, K, (0, 1, 2, 3, 4))
+    stage_evs, _ = _event_pass(torch, P, st, K, (0, 1, 2, 3, 4), split=True)
     P.pulse_decode_layer(step)  # untimed: leaves this step's recall statistics and tables in place
     torch.cuda.synchronize()
-    stage = {"score": [], "select": [], "recall": [], "attention": [], "layer": []}
+    stage = {"score": [], "select": [], "recall": [], "attention": [], "attention_kernel": [],
+             "attention_combine": [], "layer": []}
     for e in stage_evs:
         stage["score"].append(e.elapsed_ms(0, 1))
         stage["select"].append(e.elapsed_ms(1, 2))
         stage["recall"].append(e.elapsed_ms(2, 3))
         stage["attention"].append(e.elapsed_ms(3, 4))
+        stage["attention_kernel"].append(e.elapsed_ms(3, 5))
+        stage["attention_combine"].append(e.elapsed_ms(5, 4))
         stage["layer"].append(e.elapsed_ms(0, 4))
     for e in evs + chain_evs + stage_evs:
         e.destroy()
@@ -432,14 +444,17 @@ def rooflines(w, st, timed, mean, rbytes, peak_measured):
     sel = st.sel_cnt.cpu().numpy()
     attn_bytes = int(sel.sum()) * w.unit_bytes + w.q.nbytes + w.B * w.Hq * w.d * 4
     digest_bytes = int(sum(max(0, n - w.n_sink - w.n_local) for n in w.n_blocks.tolist())) * 2 * w.d * 2
-    attn = attn_bytes / (mean["attention"] * 1e-3) / 1e9
+    attn = attn_bytes / (mean["attention_kernel"] * 1e-3) / 1e9
+    attn_call = attn_bytes / (mean["attention"] * 1e-3) / 1e9
     score = digest_bytes / (mean["score"] * 1e-3) / 1e9
     roof = {"bound": "host_link", "kernel": "recall_copy_kernel", "achieved": recall_GBps, "peak": PCIE5_X16_GBPS,
             "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS, "peak_measured": peak_measured,
             "frac_of_measured": (recall_GBps / peak_measured) if peak_measured else None,
             "bytes_per_launch": rbytes}
     attn_roof = {"bound": "hbm", "kernel": "attn_splitk_kernel", "achieved": attn, "peak": HBM_GBPS, "unit": "GB/s",
-                 "frac": attn / HBM_GBPS, "bytes_per_launch": attn_bytes}
+                 "frac": attn / HBM_GBPS, "bytes_per_launch": attn_bytes,
+                 "with_combine": {"achieved": attn_call, "frac": attn_call / HBM_GBPS,
+                                  "us": mean["attention"] * 1e3, "combine_us": mean["attention_combine"] * 1e3}}
     score_roof = {"bound": "hbm", "kernel": "score_kernel", "achieved": score, "peak": HBM_GBPS, "unit": "GB/s",
                   "frac": score / HBM_GBPS, "bytes_per_launch": digest_bytes}
     return roof, attn_roof, score_roof

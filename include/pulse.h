@@ -396,6 +396,11 @@ typedef struct {
                                  overwrite.  A recall made by pulse_recall_gather or
                                  the engine is released with pulse_release_recalled.
                                  0: no release */
+    void* attn_split_event;   /* optional hipEvent_t recorded between the split-K
+                                 attention kernel and the kernel that merges its
+                                 workgroup partials (right after the attention kernel
+                                 when no merge is needed), so the split-K kernel can be
+                                 timed alone; NULL = not recorded */
 } pulse_layer_args;
 
 /*

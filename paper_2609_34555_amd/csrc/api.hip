@@ -387,7 +387,7 @@ hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs) {
     const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
     return launch_attention(a.shape, a.q, a.slot_pool, a.n_slots, a.block_table, a.max_blocks, a.sel_idx, a.sel_cnt,
                             a.k_max, a.ctx_len, a.B, a.sm_scale, a.out, a.lse, at<float>(a.ws, w.attn_o),
-                            at<float2>(a.ws, w.attn_ml), a.dev_status, hs);
+                            at<float2>(a.ws, w.attn_ml), a.dev_status, hs, (hipEvent_t)a.attn_split_event);
 }
 
 // Full argument check of a chained layer-step.

@@ -402,7 +402,7 @@ static void launch_attn_t(dim3 grid, size_t lds, hipStream_t st, const void* q, 
 hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
                             const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
                             int32_t k_max, const int32_t* ctx_len, int32_t B, float sm_scale, float* out, float* lse,
-                            float* ws_o, float2* ws_ml, int32_t* status, hipStream_t st) {
+                            float* ws_o, float2* ws_ml, int32_t* status, hipStream_t st, hipEvent_t split_done) {
     if (B == 0) return hipSuccess;
     const int32_t Hkv = s.num_kv_heads, Hq = s.num_q_heads, G = Hq / Hkv;
     const AttnPlan p = attn_plan(B, Hkv, k_max, s.block_size);
@@ -428,6 +428,7 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
 #undef PULSE_ATTN_W
 #undef PULSE_ATTN
     hipError_t e = hipGetLastError();
+    if (e == hipSuccess && split_done) e = hipEventRecord(split_done, st);
     if (e != hipSuccess || n_wg <= 1) return e;
     hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)G, (unsigned)Hkv, (unsigned)B), dim3(kCombineThreads), 0,
                        st, ws_o, ws_ml, sel_cnt, k_max, Hq, Hkv, G, p.entries_per_split, n_wg, W, out, lse);

@@ -194,7 +194,7 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
                             const int32_t* table, int32_t max_blocks, const int32_t* sel_idx,
                             const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t B,
                             float sm_scale, float* out, float* lse, float* ws_o, float2* ws_ml,
-                            int32_t* status, hipStream_t st);
+                            int32_t* status, hipStream_t st, hipEvent_t split_done = nullptr);
 
 hipError_t launch_average_scores(const float* sc, int64_t total_blocks, int32_t H, float* avg, hipStream_t st);
 hipError_t launch_mam_selection(const int32_t* ctx_len, int32_t B, int32_t bs, int32_t max_blocks, int32_t n_sink,

@@ -142,6 +142,9 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     __shared__ uint32_t wave_tot[kCopyThreads / kWave];
     __shared__ uint32_t sh_runs, sh_bad;
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    // the free-list head snapshot is read with the counts, not after the scan: the
+    // first chunk's slot lookup depends on it
+    const int32_t fh0 = misc[0];
     // exclusive scan of miss_cnt: thread t owns a contiguous segment
     const int per = (B + kCopyThreads - 1) / kCopyThreads;
     const int s0 = tid * per, s1 = min(B, s0 + per);
@@ -170,7 +173,6 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     if (tid == kCopyThreads - 1) off[B] = (int32_t)before;
     __syncthreads();
     const int64_t total = off[B];
-    const int32_t fh0 = misc[0];
     const bool ok = sh_bad == 0;
     const bool fits = fh0 >= 0 && fh0 <= n_free && total <= (int64_t)n_free - fh0;
     if (blockIdx.x == 0 && tid == 0) {

@@ -98,13 +98,18 @@ __device__ inline uint32_t block_sum(uint32_t v, ScanLds& sl) {
 // grid = (B, heads): blockIdx.x = request, blockIdx.y = selecting head slot
 // (always 0 for SoloHead; 0..Hkv-1 for headwise selection, whose per-head
 // scores, selections and plans are stacked along the head dimension).
+//
+// Requests of at most kKeyCache blocks (the cached path) keep the key of
+// block j in skey[j]; the radix passes read each thread's keys from registers
+// and the ordered pass forms its masks without branches.  Longer requests
+// re-read their scores from memory in every pass.
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int64_t* __restrict__ blk_off, int32_t B, int64_t total_blocks, const float* __restrict__ scores,
     const int32_t* __restrict__ k_mid, int32_t n_sink, int32_t n_local, int32_t k_max, int32_t* __restrict__ sel_idx,
     int32_t* __restrict__ sel_cnt, const int32_t* __restrict__ table, int32_t max_blocks, int32_t n_slots,
     const int32_t* __restrict__ free_head, int32_t* __restrict__ miss_list, int32_t* __restrict__ miss_cnt,
     int32_t* __restrict__ run_cnt, int32_t* __restrict__ req_err, int32_t* __restrict__ misc, int32_t* status) {
-    __shared__ uint32_t skey[kKeyCache];
+    __shared__ __align__(16) uint32_t skey[kKeyCache];  // key of block j at [j] (cached path)
     __shared__ uint32_t hist[256];
     __shared__ uint32_t sh_prefix, sh_kk;
     __shared__ bool sh_whole;
@@ -124,6 +129,28 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         miss_cnt += (size_t)hy * B;
         run_cnt += (size_t)hy * B;
         req_err += (size_t)hy * B;
+    }
+    // Loads issued before the request's extent is known, so that the common case
+    // costs one memory round trip: this thread's table entries of the first
+    // super-tile (blocks 8t .. 8t+7, any that exist in the row), and the scores
+    // at the offsets the request has when all requests are equally long (a wrong
+    // guess is reloaded once blk_off is known).
+    int32_t tpre[kPerThread];
+#pragma unroll
+    for (int u = 0; u < kPerThread; ++u) {
+        const int j = kPerThread * tid + u;
+        tpre[u] = (plan && j < max_blocks) ? table[(size_t)r * max_blocks + j] : -1;
+    }
+    const int64_t n_eq = total_blocks / B;
+    const int64_t b0_eq = (int64_t)r * n_eq;
+    const bool spec = n_eq >= 1 && n_eq <= kKeyCache;
+    float sv[kPerThread];
+    if (spec) {
+#pragma unroll
+        for (int u = 0; u < kPerThread; ++u) {
+            const int j = tid + u * kSelThreads;
+            sv[u] = scores[b0_eq + (j < n_eq ? j : n_eq - 1)];
+        }
     }
     const int64_t b0 = blk_off[r];
     const int64_t n = blk_off[r + 1] - b0;
@@ -147,47 +174,43 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         return;
     }
 
-    const bool cached = nc <= kKeyCache;
-    // table entries of this thread's first kPerThread blocks (8*tid ..), loaded
-    // now so their latency overlaps the threshold search
+    const bool cached = n <= kKeyCache;
     const int64_t t_lim = n < max_blocks ? n : max_blocks;  // table entries that exist
-    int32_t tpre[kPerThread];
-#pragma unroll
-    for (int u = 0; u < kPerThread; ++u) {
-        const int64_t j = (int64_t)kPerThread * tid + u;
-        tpre[u] = -1;
-        if (plan && j < t_lim) tpre[u] = table[(size_t)r * max_blocks + j];
-    }
-    const float* msc = scores + b0 + lo;  // middle scores
+    const float* rsc = scores + b0;                          // this request's scores, by block
     const bool all_mid = (k == nc);
     const bool none_mid = (k == 0);
     // Threshold: a middle block is taken if its masked offset (key - key_base) & T_mask
     // is above T, or equal to T and fewer than need_eq equal ones precede it.
     // All keys equal: T_mask = 0, so every key is "equal" and the first k are taken.
     uint32_t key_base = 0, T = 0, T_mask = 0, need_eq = (uint32_t)k;
+    // cached path: keys of blocks tid + 1024u in registers, mid_l = those that are middle
+    uint32_t kreg[kPerThread];
+    uint32_t mid_l = 0;
     if (!all_mid && !none_mid) {
-        // keys to LDS, with the block-wide min and max key
         uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-        if (cached) {  // all loads in flight at once
+        if (cached) {
+            const bool hit = spec && b0 == b0_eq && n == n_eq;
             float v[kPerThread];
 #pragma unroll
-            for (int u = 0; u < kPerThread; ++u) {  // nc >= 1 here; clamped, unconditional loads
-                const int64_t i = tid + (int64_t)u * kSelThreads;
-                v[u] = msc[i < nc ? i : nc - 1];
+            for (int u = 0; u < kPerThread; ++u) {  // n >= nc >= 1 here; clamped loads
+                const int j = tid + u * kSelThreads;
+                v[u] = hit ? sv[u] : rsc[j < n ? j : n - 1];
             }
 #pragma unroll
             for (int u = 0; u < kPerThread; ++u) {
-                const int64_t i = tid + (int64_t)u * kSelThreads;
-                if (i < nc) {
-                    const uint32_t key = key32(v[u]);
-                    skey[i] = key;
+                const int j = tid + u * kSelThreads;
+                const uint32_t key = key32(v[u]);
+                kreg[u] = key;
+                if (j < n) skey[j] = key;
+                if (j >= lo && j < hi) {
+                    mid_l |= 1u << u;
                     kmin = min(kmin, key);
                     kmax = max(kmax, key);
                 }
             }
         } else {
-            for (int64_t i = tid; i < nc; i += kSelThreads) {
-                const uint32_t key = key32(msc[i]);
+            for (int64_t j = lo + tid; j < hi; j += kSelThreads) {
+                const uint32_t key = key32(rsc[j]);
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
             }
@@ -215,9 +238,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                 const uint32_t dmask = shift >= 0 ? 255u : (255u >> -shift);
                 if (tid < 256) hist[tid] = 0;
                 __syncthreads();
-                for (int64_t i = tid; i < nc; i += kSelThreads) {
-                    const uint32_t off = (cached ? skey[i] : key32(msc[i])) - kmin;
-                    if ((off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
+                if (cached) {
+#pragma unroll
+                    for (int u = 0; u < kPerThread; ++u) {
+                        const uint32_t off = kreg[u] - kmin;
+                        if (((mid_l >> u) & 1u) && (off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
+                    }
+                } else {
+                    for (int64_t j = lo + tid; j < hi; j += kSelThreads) {
+                        const uint32_t off = key32(rsc[j]) - kmin;
+                        if ((off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
+                    }
                 }
                 __syncthreads();
                 if (wid == 0) {
@@ -259,23 +290,41 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     uint32_t eq_carry = 0, sel_carry = 0, miss_carry = 0, runs = 0, prev_bit = 0;
     int32_t my_err = 0;
     const bool thr = !all_mid && !none_mid;
+    // bits u of [0, 8) with a <= j0 + u < b
+    auto range_mask = [](int64_t a, int64_t b, int64_t j0) -> uint32_t {
+        const int64_t a_rel = a - j0, b_rel = b - j0;
+        const uint32_t ac = a_rel <= 0 ? 0u : (a_rel >= kPerThread ? (uint32_t)kPerThread : (uint32_t)a_rel);
+        const uint32_t bc = b_rel <= 0 ? 0u : (b_rel >= kPerThread ? (uint32_t)kPerThread : (uint32_t)b_rel);
+        return ((1u << bc) - 1u) & ~((1u << ac) - 1u);
+    };
     for (int64_t base = 0; base < n; base += (int64_t)kSelThreads * kPerThread) {
         const int64_t j0 = base + (int64_t)kPerThread * tid;
-        uint32_t forced_m = 0, gt_m = 0, eq_m = 0;
+        const uint32_t valid_m = range_mask(0, n, j0);
+        const uint32_t mid_m = range_mask(lo, hi, j0);
+        const uint32_t forced_m = valid_m & ~mid_m;
+        uint32_t gt_m = 0, eq_m = 0;
+        if (all_mid) {
+            gt_m = mid_m;
+        } else if (thr && mid_m) {
+            uint32_t kb[kPerThread];
+            if (cached) {  // j0 + 7 < kKeyCache: two 16-byte LDS reads
+                const u32x4 a = *reinterpret_cast<const u32x4*>(&skey[j0]);
+                const u32x4 b = *reinterpret_cast<const u32x4*>(&skey[j0 + 4]);
 #pragma unroll
-        for (int u = 0; u < kPerThread; ++u) {
-            const int64_t j = j0 + u;
-            if (j >= n) break;
-            if (j < lo || j >= hi) {
-                forced_m |= 1u << u;
-            } else if (all_mid) {
-                gt_m |= 1u << u;
-            } else if (thr) {
-                const uint32_t key = cached ? skey[j - lo] : key32(msc[j - lo]);
-                const uint32_t mo = (key - key_base) & T_mask;
+                for (int i = 0; i < 4; ++i) { kb[i] = a[i]; kb[4 + i] = b[i]; }
+            } else {
+#pragma unroll
+                for (int u = 0; u < kPerThread; ++u)
+                    kb[u] = ((mid_m >> u) & 1u) ? key32(rsc[j0 + u]) : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < kPerThread; ++u) {
+                const uint32_t mo = (kb[u] - key_base) & T_mask;
                 gt_m |= (uint32_t)(mo > T) << u;
                 eq_m |= (uint32_t)(mo == T) << u;
             }
+            gt_m &= mid_m;
+            eq_m &= mid_m;
         }
         // scan 1: equal keys before this thread's blocks
         uint32_t eq_tot;

@@ -74,7 +74,7 @@ class pulse_layer_args(ctypes.Structure):
         ("free_slots", _P), ("free_head", _P), ("n_free", ctypes.c_int32), ("slot_pool", _P),
         ("n_slots", ctypes.c_int32), ("stats", _P), ("sm_scale", ctypes.c_float), ("out", _P), ("lse", _P),
         ("dev_status", _P), ("ws", _P), ("ws_bytes", ctypes.c_size_t), ("events", _P),
-        ("release_previous", ctypes.c_int32),
+        ("release_previous", ctypes.c_int32), ("attn_split_event", _P),
     ]
 
 
