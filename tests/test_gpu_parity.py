@@ -71,6 +71,9 @@ SELECT_CASES = [
     ("big_n", [131072, 70000], 32, 8, 16, "bf16", [247, 100], 1, 8),
     # > 8192 middle blocks: keys re-read from L2 each radix pass, two ordered super-tiles
     ("uncached_two_tiles", [150000, 140000, 3000], 32, 8, 16, "bf16", [300, 5, 40], 1, 8),
+    # 100 / 140 / 60 / 100 blocks: the equal-length guess of the score and select kernels
+    # (100 blocks each) holds for requests 0 and 3 and fails for 1 (length) and 2 (offset)
+    ("equal_length_guess", [1600, 2240, 960, 1585], 32, 8, 16, "bf16", [20, 31, 9, 50], 1, 8),
 ]
 
 
@@ -107,6 +110,17 @@ def test_chained_layer_beyond_key_cache():
     w, st = build(spec, s)
     res = full_check(w, st, chained=True)
     say(f"  attn max err {res['attn_err']}")
+
+
+def test_chained_layer_equal_length_guess():
+    """A chained layer-step on requests of 100 / 140 / 60 / 100 blocks: the kernels' loads at
+    equal-length offsets are used for requests 0 and 3 and reloaded for 1 and 2."""
+    spec, s = W.custom("eqguess", [1600, 2240, 960, 1585], Hq=32, Hkv=8, bs=16, dtype="bf16", k_mid=[20, 31, 9, 50],
+                       n_sink=1, n_local=8, resident_frac=0.1, heavy_per_req=6)
+    w, st = build(spec, s)
+    assert w.total_blocks == 400 and list(w.n_blocks) == [100, 140, 60, 100]
+    res = full_check(w, st, chained=True)
+    say(f"  stats={res['stats']} attn max err {res['attn_err']}")
 
 
 def test_chained_layer_at_maximum_batch():
@@ -307,12 +321,14 @@ def test_decode_layer_stage_events_all_some_none():
     spec, s = W.preset(2, ctx_scale=1 / 8)
     w, st = build(spec, s)
     outs = []
-    sets = [P.EventSet(5) for _ in range(3)]
+    sets = [P.EventSet(6) for _ in range(3)]
     try:
         for keep in (None, (0, 1, 2, 3, 4), (2, 3)):
             a = st.layer_args()
             if keep is not None:
                 a.events = sets[len(outs)].masked_ptr(keep)
+            if keep == (0, 1, 2, 3, 4):  # and the one between the split-K kernel and its combine
+                a.attn_split_event = sets[len(outs)].arr[5]
             st.reset()
             assert P.pulse_decode_layer(a) == 0
             torch.cuda.synchronize()
@@ -323,6 +339,7 @@ def test_decode_layer_stage_events_all_some_none():
         for e in sets[1:]:
             assert e.elapsed_ms(2, 3) > 0.0
         assert sets[1].elapsed_ms(0, 4) >= sets[1].elapsed_ms(2, 3)
+        assert 0.0 < sets[1].elapsed_ms(3, 5) <= sets[1].elapsed_ms(3, 4)
     finally:
         for e in sets:
             e.destroy()
