@@ -148,6 +148,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     if (spec) {
 #pragma unroll
         for (int u = 0; u < kPerThread; ++u) {
+            if (u * kSelThreads >= n_eq) break;  // workgroup-uniform: no key of this slot exists
             const int j = tid + u * kSelThreads;
             sv[u] = scores[b0_eq + (j < n_eq ? j : n_eq - 1)];
         }
@@ -193,11 +194,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
             float v[kPerThread];
 #pragma unroll
             for (int u = 0; u < kPerThread; ++u) {  // n >= nc >= 1 here; clamped loads
+                if (u * kSelThreads >= n) break;
                 const int j = tid + u * kSelThreads;
                 v[u] = hit ? sv[u] : rsc[j < n ? j : n - 1];
             }
 #pragma unroll
             for (int u = 0; u < kPerThread; ++u) {
+                if (u * kSelThreads >= n) break;
                 const int j = tid + u * kSelThreads;
                 const uint32_t key = key32(v[u]);
                 kreg[u] = key;
@@ -241,6 +244,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                 if (cached) {
 #pragma unroll
                     for (int u = 0; u < kPerThread; ++u) {
+                        if (u * kSelThreads >= n) break;
                         const uint32_t off = kreg[u] - kmin;
                         if (((mid_l >> u) & 1u) && (off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
                     }
