@@ -37,3 +37,34 @@ def test_threaded_oracle_step_matches_whole_batch():
 def test_host_info_fields():
     info = bench.host_info()
     assert info["nproc"] >= 1 and 1 <= info["usable_cpus"] <= info["nproc"]
+
+
+def test_more_than_one_gpu_is_refused():
+    """The benchmark measures one GPU; asking for more exits with a message, before any GPU work."""
+    import subprocess
+    import sys
+
+    res = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True, timeout=120)
+    assert res.returncode != 0 and "one GPU" in res.stderr and res.stdout == ""
+
+
+def test_counter_traffic_only_for_unchanged_sources(tmp_path, monkeypatch):
+    """Byte counters are reported for a kernel only while its sources hash as when they were
+    collected; any other hash, or a kernel with no counters, gives None."""
+    import hashlib
+    import json
+
+    src = tmp_path / "k.hip"
+    src.write_text("kernel source\n")
+    good = hashlib.sha256(src.read_bytes()).hexdigest()[:16]
+    data = {"kernels": {
+        "same": {"fetch_bytes": 3.0, "write_bytes": 4.0, "sources": ["k.hip"], "sources_sha256_16": good},
+        "changed": {"fetch_bytes": 3.0, "write_bytes": 4.0, "sources": ["k.hip"], "sources_sha256_16": "0" * 16}}}
+    (tmp_path / "profiles").mkdir()
+    (tmp_path / "profiles" / "counters_cfg2.json").write_text(json.dumps(data))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.counter_traffic("same") == {"fetch": 3.0, "write": 4.0, "total": 7.0}
+    assert bench.counter_traffic("changed") is None
+    assert bench.counter_traffic("absent") is None
+    src.write_text("edited\n")
+    assert bench.counter_traffic("same") is None
