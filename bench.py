@@ -704,7 +704,7 @@ def bench_ioaa(args, torch, P, H):
     digest_bytes = (16384 // 16) * 2 * 128 * 2 * 32  # one head's per-block min/max, 32 layers, 16K tokens
     params = P.make_ioaa_params(40 << 30, kv_per_token, 2048, digest_bytes, 32, 8, grid_bo, grid_bn, m)
     t = time.perf_counter()
-    assign, thr, nodes = P.pulse_ioaa_plan(params, lengths)
+    assign, thr, nodes, leaves = P.pulse_ioaa_plan(params, lengths)
     plan_us = (time.perf_counter() - t) * 1e6
     return {"report": "ioaa", "grid_bo": grid_bo, "grid_bn": grid_bn, "overlap_depth": m.tolist(),
             "grid_detail": detail, "measured_with": "pulse_irq_step semi_sync + pulse_gs engine, 8 layers, "
@@ -713,6 +713,7 @@ def bench_ioaa(args, torch, P, H):
                       "running_normal": 32, "running_offload": 8},
             "plan": {"normal": int((assign == 1).sum()), "offload": int((assign == 2).sum()),
                      "wait": int((assign == 0).sum()), "throughput_eq1": thr, "nodes_visited": nodes,
+                     "assignments_evaluated": leaves,
                      "plan_us": plan_us}}
 
 

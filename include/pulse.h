@@ -546,11 +546,16 @@ PULSE_API double pulse_overlap_depth(const pulse_ioaa_params* params, double b_o
  * and no offloading after a longer request went to the normal batch.  A request
  * that fits neither batch ends its path (it and all shorter ones wait).
  *   assign[i] = 0 wait, 1 normal, 2 offload (host array); *throughput = Eq. 1
- *   at the chosen assignment; *nodes_visited (optional) = search nodes.
+ *   at the chosen assignment; *nodes_visited (optional) = tree nodes the search
+ *   visits; *leaves_evaluated (optional) = complete assignments at which it
+ *   evaluates Eq. 1 (the admissible ones; a root-to-leaf path of n requests
+ *   alone passes n + 1 nodes, so this is the count comparable with the
+ *   paper's nodes-visited figure).
  * Host-only; no GPU work.
  */
 PULSE_API pulse_status pulse_ioaa_plan(const pulse_ioaa_params* params, const int64_t* lengths, int32_t n,
-                                       int8_t* assign, double* throughput, int64_t* nodes_visited);
+                                       int8_t* assign, double* throughput, int64_t* nodes_visited,
+                                       int64_t* leaves_evaluated);
 
 /* ---- measurement helpers (host side; not part of the compute path) ---- */
 

@@ -56,14 +56,13 @@ def throughput(b_n, b_o, m):
     return m / (m + 1.0) * b_n + 1.0 / (m + 1.0) * b_o
 
 
-def best_assignment(lengths, budget, kv_bytes_per_token, offload_tokens, offload_extra, run_n, run_o, grid_bo,
-                    grid_bn, grid_m):
-    """Enumerate every admissible assignment; returns (assign [n] in {0 wait, 1 normal,
-    2 offload}, throughput).  Ties keep the assignment with the most normal admissions,
-    then the most offloads (any maximiser is accepted by the tests when values tie)."""
+def admissible(lengths, budget, kv_bytes_per_token, offload_tokens, offload_extra):
+    """Every admissible assignment, as (order, choice): the first len(choice) requests of
+    `order` (longest first) are decided (1 normal, 2 offload), the rest wait.  Admissible:
+    within the memory budget, no offload after a longer normal request (Sec. 4.3.1), and
+    waiting only where the next request fits neither batch (I1)."""
     n = len(lengths)
     order = sorted(range(n), key=lambda i: (-lengths[i], i))
-    best, best_thr = None, -1.0
     for k in range(n + 1):  # the first k requests (longest first) are decided, the rest wait
         for choice in itertools.product((1, 2), repeat=k):
             if any(choice[t] == 2 and 1 in choice[:t] for t in range(k)):
@@ -85,12 +84,29 @@ def best_assignment(lengths, budget, kv_bytes_per_token, offload_tokens, offload
                 can_o = cost_o <= budget and 1 not in choice
                 if can_n or can_o:
                     continue
-            b_n = run_n + sum(1 for c in choice if c == 1)
-            b_o = run_o + sum(1 for c in choice if c == 2)
-            thr = throughput(b_n, b_o, overlap_depth(grid_bo, grid_bn, grid_m, b_o, b_n))
-            if thr > best_thr:
-                best_thr = thr
-                best = [0] * n
-                for t in range(k):
-                    best[order[t]] = choice[t]
+            yield order, choice
+
+
+def count_admissible(lengths, budget, kv_bytes_per_token, offload_tokens, offload_extra):
+    """Number of admissible assignments: the complete assignments at which a search over
+    the pruned tree evaluates Eq. 1."""
+    return sum(1 for _ in admissible(lengths, budget, kv_bytes_per_token, offload_tokens, offload_extra))
+
+
+def best_assignment(lengths, budget, kv_bytes_per_token, offload_tokens, offload_extra, run_n, run_o, grid_bo,
+                    grid_bn, grid_m):
+    """Enumerate every admissible assignment; returns (assign [n] in {0 wait, 1 normal,
+    2 offload}, throughput).  Ties keep the assignment with the most normal admissions,
+    then the most offloads (any maximiser is accepted by the tests when values tie)."""
+    n = len(lengths)
+    best, best_thr = None, -1.0
+    for order, choice in admissible(lengths, budget, kv_bytes_per_token, offload_tokens, offload_extra):
+        b_n = run_n + sum(1 for c in choice if c == 1)
+        b_o = run_o + sum(1 for c in choice if c == 2)
+        thr = throughput(b_n, b_o, overlap_depth(grid_bo, grid_bn, grid_m, b_o, b_n))
+        if thr > best_thr:
+            best_thr = thr
+            best = [0] * n
+            for t in range(len(choice)):
+                best[order[t]] = choice[t]
     return best, best_thr

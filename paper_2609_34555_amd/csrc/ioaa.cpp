@@ -26,7 +26,8 @@ struct Search {
     std::vector<int64_t> len;  // sorted longest first
     std::vector<int8_t> cur, best;
     double best_thr = -1.0;
-    int64_t nodes = 0;
+    int64_t nodes = 0;   // tree nodes visited
+    int64_t leaves = 0;  // complete assignments at which Eq. 1 is evaluated
 
     double depth(double b_o, double b_n) const { return pulse_overlap_depth(p, b_o, b_n); }
 
@@ -37,6 +38,7 @@ struct Search {
     }
 
     void leaf(int64_t nn, int64_t no) {
+        ++leaves;
         const double t = thr(p->running_normal + nn, p->running_offload + no);
         if (t > best_thr) {
             best_thr = t;
@@ -105,7 +107,7 @@ double pulse_overlap_depth(const pulse_ioaa_params* p, double b_o, double b_n) {
 }
 
 pulse_status pulse_ioaa_plan(const pulse_ioaa_params* p, const int64_t* lengths, int32_t n, int8_t* assign,
-                             double* throughput, int64_t* nodes_visited) {
+                             double* throughput, int64_t* nodes_visited, int64_t* leaves_evaluated) {
     if (!p || n < 0 || (n > 0 && (!lengths || !assign)) || !throughput) return PULSE_ERR_INVALID_ARG;
     if (!p->grid_bo || !p->grid_bn || !p->grid_m || p->n_bo < 1 || p->n_bn < 1) return PULSE_ERR_INVALID_ARG;
     for (int i = 1; i < p->n_bo; ++i)
@@ -128,6 +130,7 @@ pulse_status pulse_ioaa_plan(const pulse_ioaa_params* p, const int64_t* lengths,
     for (int i = 0; i < n; ++i) assign[order[i]] = s.best[i];
     *throughput = s.best_thr;
     if (nodes_visited) *nodes_visited = s.nodes;
+    if (leaves_evaluated) *leaves_evaluated = s.leaves;
     return PULSE_OK;
 }
 

@@ -161,7 +161,8 @@ def lib():
             "pulse_overlap_depth": (ctypes.c_double, [ctypes.POINTER(pulse_ioaa_params), ctypes.c_double,
                                                       ctypes.c_double]),
             "pulse_ioaa_plan": (ctypes.c_int, [ctypes.POINTER(pulse_ioaa_params), _P, I32, _P,
-                                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64)]),
+                                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
+                                               ctypes.POINTER(ctypes.c_int64)]),
             "pulse_events_create": (ctypes.c_int, [I32, _P]),
             "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
             "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
@@ -410,17 +411,20 @@ def pulse_overlap_depth(params: pulse_ioaa_params, b_o: float, b_n: float) -> fl
 
 
 def pulse_ioaa_plan(params: pulse_ioaa_params, lengths):
-    """Returns (assign int8 [n]: 0 wait / 1 normal / 2 offload, throughput, nodes_visited)."""
+    """Returns (assign int8 [n]: 0 wait / 1 normal / 2 offload, throughput, nodes_visited,
+    leaves_evaluated)."""
     import numpy as np
 
     L = np.ascontiguousarray(lengths, dtype=np.int64)
     assign = np.zeros(L.size, np.int8)
     thr = ctypes.c_double()
     nodes = ctypes.c_int64()
+    leaves = ctypes.c_int64()
     _check(lib().pulse_ioaa_plan(ctypes.byref(params), L.ctypes.data if L.size else None, L.size,
-                                 assign.ctypes.data if L.size else None, ctypes.byref(thr), ctypes.byref(nodes)),
+                                 assign.ctypes.data if L.size else None, ctypes.byref(thr), ctypes.byref(nodes),
+                                 ctypes.byref(leaves)),
            "pulse_ioaa_plan", True)
-    return assign, thr.value, nodes.value
+    return assign, thr.value, nodes.value, leaves.value
 
 
 class GatherScatterEngine:

@@ -75,8 +75,10 @@ def test_library_search_equals_exhaustive_oracle(seed):
     m = rng.uniform(1, 6, (4, 3))
     want, want_thr = OI.best_assignment(lengths, budget, 1, hot, extra, rn, ro, bo, bn, m)
     p = _params(budget, 1, hot, extra, rn, ro, bo, bn, m)
-    got, thr, nodes = P.pulse_ioaa_plan(p, lengths)
+    got, thr, nodes, leaves = P.pulse_ioaa_plan(p, lengths)
     assert thr == pytest.approx(want_thr, rel=1e-12, abs=1e-12)
+    # Eq. 1 is evaluated exactly at the admissible assignments, each once
+    assert leaves == OI.count_admissible(lengths, budget, 1, hot, extra)
     # the library's assignment is admissible and reaches that throughput
     order = sorted(range(n), key=lambda i: (-lengths[i], i))
     mem, seen_normal, b_n, b_o = 0, False, rn, ro
@@ -100,21 +102,25 @@ def test_library_search_equals_exhaustive_oracle(seed):
 
 def test_pruned_search_is_small_under_memory_pressure():
     """30 waiting requests of lognormal lengths, GPU room for a few long ones: the two prunes
-    keep the walk to a few nodes per request (about 18 on average here; the paper reports
-    3.16 on average for 30 waiting requests on its own serving trace, Sec. 4.3.1)."""
+    keep the walk to a few nodes per request, and Eq. 1 is evaluated at a handful of
+    complete assignments (the paper reports 3.16 nodes visited on average for 30 waiting
+    requests of its own serving trace, Sec. 4.3.1; a root-to-leaf path alone passes 31
+    nodes, so its figure is comparable with the evaluated assignments)."""
     rng = np.random.default_rng(0)
     bo = [1.0, 4.0, 16.0, 64.0]
     bn = [1.0, 16.0, 64.0]
     m = [[1.0, 1.0, 1.0], [1.5, 1.3, 1.2], [3.0, 2.5, 2.2], [9.0, 8.0, 7.0]]
-    counts = []
+    counts, evaluated = [], []
     for _ in range(50):
         lengths = np.clip(rng.lognormal(np.log(16384), 1.0, 30), 256, 262144).astype(np.int64)
         budget = int(rng.uniform(0.5, 3.0) * 16384 * 160 * 1024)  # room for a few long requests
         p = _params(budget, 160 * 1024, 2048, 1 << 20, 8, 4, bo, bn, m)
-        _, _, nodes = P.pulse_ioaa_plan(p, lengths)
+        _, _, nodes, leaves = P.pulse_ioaa_plan(p, lengths)
         counts.append(nodes)
+        evaluated.append(leaves)
     assert np.mean(counts) < 2 * 30  # far below the 2^30 leaves of the unpruned tree
     assert max(counts) < 4 * 30
+    assert 1 <= min(evaluated) and np.mean(evaluated) < 10
 
 
 def test_validation():
