@@ -44,6 +44,9 @@ def parse():
                          "resident normal batch, every detection mode and both recall paths (not the default line)")
     ap.add_argument("--ioaa-profile", action="store_true",
                     help="report: overlap depth measured over a (B_o, B_n) grid and an IOAA admission on it")
+    ap.add_argument("--recall-sweep", action="store_true",
+                    help="report: recall bandwidth against the number of blocks per recall for the GPU gather "
+                         "kernel, the paper's engine and one hipMemcpyAsync per block (not the default line)")
     ap.add_argument("--normal-batch", type=int, default=32)
     ap.add_argument("--profile", action="store_true",
                     help="profiler run: no CPU baseline or link probes; adds one 256 MiB device copy "
@@ -717,6 +720,83 @@ def bench_ioaa(args, torch, P, H):
                      "plan_us": plan_us}}
 
 
+def bench_recall_sweep(args, torch, P, H, W):
+    """Recall bandwidth against the number of blocks recalled in one call (the analogue of the
+    paper's gather-scatter figure, Sec. 4.4.2): the preset's selection is cut down to its first
+    n missing blocks (request order, block order), and the same blocks are recalled by the GPU
+    gather kernel (pulse_recall_gather: plan + copy, HIP events), the paper's engine (submit to
+    host-observed completion) and one hipMemcpyAsync per block (HIP events around the calls).
+    Each recall starts from the initial table and free list; median of `reps` after a warm-up."""
+    import numpy as np
+
+    spec, seed = W.preset(args.config)
+    holder = []
+    w = W.generate(spec, seed, kv_alloc=H.pinned_allocator(holder))
+    st = H.LayerState(w, holder[0].ptr)
+    st.reset()
+    st.select()
+    torch.cuda.synchronize()
+    idx, cnt = st.selection()
+    missing = [(r, int(j)) for r in range(w.B) for j in idx[r, : cnt[r]] if w.table0[r, j] < 0]
+    reps = 7
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    eng = P.GatherScatterEngine(st.shape, n_workers=8, max_blocks_per_call=w.B * st.k_max,
+                                staging_blocks=max(1, (16 << 20) // w.unit_bytes))
+    sizes = [n for n in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 2048, 4096) if n < len(missing)]
+    sizes.append(len(missing))
+    rows = []
+    try:
+        for n in sizes:
+            keep = set(missing[:n])
+            sel = np.full_like(idx, -1)
+            c = np.zeros_like(cnt)
+            for r in range(w.B):  # the cut selection: its resident blocks and its first n missing ones
+                js = [int(j) for j in idx[r, : cnt[r]] if w.table0[r, j] >= 0 or (r, int(j)) in keep]
+                sel[r, : len(js)] = js
+                c[r] = len(js)
+            st.sel_idx.copy_(torch.from_numpy(sel))
+            st.sel_cnt.copy_(torch.from_numpy(c))
+            src = np.array([w.blk_off[r] + j for r, j in missing[:n]], np.int64)
+            dst = np.array(w.free_slots[:n], np.int64)
+            gather, engine, memcpy = [], [], []
+            for rep in range(reps + 1):
+                st.reset()
+                torch.cuda.synchronize()
+                e0.record()
+                st.recall()
+                e1.record()
+                torch.cuda.synchronize()
+                if st.recall_stats()[0] != n or st.status() != 0:
+                    raise RuntimeError(f"gather recall of {n} blocks: stats {st.recall_stats()} status {st.status()}")
+                gather.append(e0.elapsed_time(e1))
+                st.reset()
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                st.recall_gs(eng)
+                engine.append((time.perf_counter() - t0) * 1e3)
+                if st.recall_stats()[0] != n or st.status() != 0:
+                    raise RuntimeError(f"engine recall of {n} blocks: stats {st.recall_stats()} status {st.status()}")
+                e0.record()
+                P.pulse_baseline_memcpy_units(st.host_ptr, st.pool, src, dst, n, w.unit_bytes)
+                e1.record()
+                torch.cuda.synchronize()
+                memcpy.append(e0.elapsed_time(e1))
+            nbytes = n * w.unit_bytes
+            row = {"blocks": n, "bytes": nbytes}
+            for name, t in (("gather_kernel", gather), ("engine", engine), ("per_block_memcpy", memcpy)):
+                ms = statistics.median(t[1:])
+                row[name] = {"us": ms * 1e3, "GBps": nbytes / (ms * 1e-3) / 1e9}
+            rows.append(row)
+            print(f"# {n:5d} blocks: gather {row['gather_kernel']['GBps']:6.2f}  engine {row['engine']['GBps']:6.2f}"
+                  f"  per-block memcpy {row['per_block_memcpy']['GBps']:6.2f} GB/s", file=sys.stderr, flush=True)
+    finally:
+        eng.destroy()
+    return {"report": "recall_sweep", "workload": WORKLOADS[args.config], "unit_bytes": w.unit_bytes,
+            "timing": "gather: HIP events around pulse_recall_gather (plan + copy kernels); engine: host wall time "
+                      "from submit to observed completion; per-block memcpy: HIP events around the n calls",
+            "rows": rows}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -731,6 +811,9 @@ def main():
     from paper_2609_34555_amd import workloads as W
 
     torch.cuda.set_device(0)
+    if args.recall_sweep:
+        print(json.dumps(bench_recall_sweep(args, torch, P, H, W)), flush=True)
+        return
     if args.irq or args.ioaa_profile:
         line = bench_irq(args, torch, P, H) if args.irq else bench_ioaa(args, torch, P, H)
         print(json.dumps(line), flush=True)
