@@ -508,6 +508,9 @@ def bench_layer(cid, args, torch, P, H, W):
     if cid == 2:  # the committed counter passes were taken on this workload
         roof["traffic"] = (counter_traffic("recall_copy_kernel") or {}).get("total")
         roof["traffic_split"] = counter_traffic("recall_copy_kernel")
+        if roof["traffic"] is not None:
+            roof["traffic_note"] = ("fetch = the blocks read from pinned host memory over the link, write = the "
+                                    "same bytes stored to the HBM slot pool: each is bytes_per_launch, no re-reads")
         attn_roof["traffic"] = (counter_traffic("attn_splitk_kernel") or {}).get("total")
         score_roof["traffic"] = (counter_traffic("score_kernel") or {}).get("total")
     else:
