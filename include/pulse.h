@@ -396,11 +396,12 @@ typedef struct {
                                  overwrite.  A recall made by pulse_recall_gather or
                                  the engine is released with pulse_release_recalled.
                                  0: no release */
-    void* attn_split_event;   /* optional hipEvent_t recorded between the split-K
-                                 attention kernel and the kernel that merges its
-                                 workgroup partials (right after the attention kernel
-                                 when no merge is needed), so the split-K kernel can be
-                                 timed alone; NULL = not recorded */
+    void* attn_split_event;   /* optional hipEvent_t recorded at the completion of the
+                                 split-K attention kernel, before the kernel that merges
+                                 its workgroup partials (if any): the launch carries it
+                                 as the kernel's stop event, so the split-K kernel can
+                                 be timed alone without a marker of its own; NULL = not
+                                 recorded */
 } pulse_layer_args;
 
 /*

@@ -27,6 +27,8 @@
 // per output element, with independent loads.  (Merging in the last workgroup
 // to finish would need a device-scope release fence per workgroup, which on
 // gfx950 writes back the XCD's L2 and costs more than the extra launch.)
+#include <hip/hip_ext.h>
+
 #include "pulse_internal.h"
 
 namespace pulse {
@@ -388,15 +390,23 @@ AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
     return p;
 }
 
+// With `done`, the launch carries it as the kernel's stop event (recorded by the
+// dispatch itself at the kernel's completion, so timing it adds no marker packet).
 template <int DT, int BS, int W>
-static void launch_attn_t(dim3 grid, size_t lds, hipStream_t st, const void* q, const void* pool, int32_t n_slots,
-                          const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
-                          int32_t k_max, const int32_t* ctx_len, int32_t Hq, int32_t Hkv, int32_t G, int32_t eps,
-                          int32_t n_wg, float scale_log2, float* ws_o, float2* ws_ml, float* out, float* lse,
-                          int32_t* status) {
-    hipLaunchKernelGGL((attn_splitk_kernel<DT, BS, W>), grid, dim3(W * kWave), lds, st, (const uint16_t*)q,
-                       (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq, Hkv,
-                       G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse, status);
+static void launch_attn_t(dim3 grid, size_t lds, hipStream_t st, hipEvent_t done, const void* q, const void* pool,
+                          int32_t n_slots, const int32_t* table, int32_t max_blocks, const int32_t* sel_idx,
+                          const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t Hq, int32_t Hkv,
+                          int32_t G, int32_t eps, int32_t n_wg, float scale_log2, float* ws_o, float2* ws_ml,
+                          float* out, float* lse, int32_t* status) {
+    if (done)
+        hipExtLaunchKernelGGL(attn_splitk_kernel<DT, BS, W>, grid, dim3(W * kWave), (uint32_t)lds, st, nullptr, done,
+                              0u, (const uint16_t*)q, (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx,
+                              sel_cnt, k_max, ctx_len, Hq, Hkv, G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse,
+                              status);
+    else
+        hipLaunchKernelGGL((attn_splitk_kernel<DT, BS, W>), grid, dim3(W * kWave), lds, st, (const uint16_t*)q,
+                           (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq,
+                           Hkv, G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse, status);
 }
 
 hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
@@ -412,7 +422,8 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
     const size_t lds = sizeof(float) * W * G * kHeadDim + sizeof(float2) * W * G;
     const float scale_log2 = sm_scale * 1.4426950408889634f;
 #define PULSE_ATTN(DT, BS, W)                                                                                        \
-    launch_attn_t<DT, BS, W>(grid, lds, st, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len,   \
+    launch_attn_t<DT, BS, W>(grid, lds, st, split_done, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt,      \
+                             k_max, ctx_len,                                                                        \
                              Hq, Hkv, G, p.entries_per_split, n_wg, scale_log2, ws_o, ws_ml, out, lse, status)
 #define PULSE_ATTN_W(DT, BS) \
     if (W == 8) PULSE_ATTN(DT, BS, 8); else PULSE_ATTN(DT, BS, 4)
@@ -428,7 +439,6 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
 #undef PULSE_ATTN_W
 #undef PULSE_ATTN
     hipError_t e = hipGetLastError();
-    if (e == hipSuccess && split_done) e = hipEventRecord(split_done, st);
     if (e != hipSuccess || n_wg <= 1) return e;
     hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)G, (unsigned)Hkv, (unsigned)B), dim3(kCombineThreads), 0,
                        st, ws_o, ws_ml, sel_cnt, k_max, Hq, Hkv, G, p.entries_per_split, n_wg, W, out, lse);
