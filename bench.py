@@ -324,8 +324,7 @@ def base_line(cid, K, warmup):
 def _event_pass(torch, P, st, K, keep, every=1, split=False):
     """K steps; every `every`-th layer-step records the stage events in `keep` (indices into
     the five of pulse_layer_args.events; the others are left out), the rest none; with
-    `split`, event 5 is recorded between the split-K attention kernel and its combine
-    (pulse_layer_args.attn_split_event).  Returns the EventSets of the recording steps and
+    `split`, event 5 is the split-K attention kernel's end (pulse_layer_args.attn_split_event).  Returns the EventSets of the recording steps and
     the host wall time of the K steps."""
     evs = []
     args = []
@@ -349,12 +348,12 @@ def timed_steps(torch, P, st, K, warmup):
     """W untimed steps, then exactly K timed steps, bracketed by device synchronisation.  A
     step is pulse_decode_layer with release_previous set: it first undoes the previous step's
     recall (inside the scoring kernel; the hot set stays fixed-size), so every step recalls
-    the same blocks.  Inside the timed region only the two events around
-    the recall copy (the roofline kernel) are recorded, on every 4th step: each record adds
-    ~3 us to the stream.
-    Two untimed passes of K steps follow: events before score and after attention only (the
-    chain's duration), then all five plus the one between the split-K attention kernel and
-    its combine (the per-stage split, which carries the records' cost)."""
+    the same blocks.  Inside the timed region only the recall copy kernel's start and end
+    events (the roofline kernel) are recorded, on every 4th step: the library attaches them to
+    the kernel's launch, but recording events still costs the stream some time between launches.
+    Two untimed passes of K steps follow: the scoring kernel's start and the attention's end
+    only (the chain's duration), then all five plus the split-K attention kernel's end (the
+    per-stage split)."""
     step = st.layer_args(release_previous=True)
     st.reset()  # once, untimed: nothing recalled yet
     for _ in range(warmup):
@@ -386,23 +385,24 @@ def timed_steps(torch, P, st, K, warmup):
 
 def hbm_probe(torch, P, nbytes, reps=10):
     """Read bandwidth this GPU sustains over `nbytes` of device memory: the streaming read
-    probe, each launch bracketed by its own HIP events (as the stage events bracket a
-    kernel), mean over `reps` launches after 3 warm-ups.  A spin kernel queued first keeps
-    the GPU busy while the host enqueues the launches, so no host latency is timed."""
+    probe, each launch carrying its own start and stop events (as the layer-step's stage
+    events are carried by its kernels), mean over `reps` launches after 3 warm-ups.  A spin
+    kernel queued first keeps the GPU busy while the host enqueues the launches."""
     nbytes = max(16, (int(nbytes) // 16) * 16)
     src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
     sink = torch.zeros(P.pulse_probe_hbm_sink_bytes() // 4, dtype=torch.int32, device="cuda")
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-    for _ in range(3):
-        P.pulse_probe_hbm_read(src, nbytes, sink)
-    torch.cuda.synchronize()
-    torch.cuda._sleep(20_000_000)  # ~10 ms of GPU time ahead of the enqueues below
-    for e0, e1 in evs:
-        e0.record()
-        P.pulse_probe_hbm_read(src, nbytes, sink)
-        e1.record()
-    torch.cuda.synchronize()
-    ms = statistics.mean(e0.elapsed_time(e1) for e0, e1 in evs)
+    ev = P.EventSet(2 * reps)
+    try:
+        for _ in range(3):
+            P.pulse_probe_hbm_read(src, nbytes, sink)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(20_000_000)  # ~10 ms of GPU time ahead of the enqueues below
+        for i in range(reps):
+            P.pulse_probe_hbm_read(src, nbytes, sink, start_event=ev.arr[2 * i], stop_event=ev.arr[2 * i + 1])
+        torch.cuda.synchronize()
+        ms = statistics.mean(ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(reps))
+    finally:
+        ev.destroy()
     del src, sink
     return nbytes / (ms * 1e-3) / 1e9
 

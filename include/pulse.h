@@ -381,11 +381,14 @@ typedef struct {
     int32_t* dev_status;      /* device, required */
     void* ws;
     size_t ws_bytes;
-    void* const* events;      /* optional host array of 5 hipEvent_t, recorded on the
-                                 stream before score, select, recall copy, attention and
-                                 after attention (stage timing); NULL = none, and a NULL
-                                 entry is not recorded (each record adds a few
-                                 microseconds to the stream) */
+    void* const* events;      /* optional host array of 5 hipEvent_t for stage timing:
+                                 [0] start and [1] end of the scoring kernel, [2] start
+                                 and [3] end of the recall copy kernel, [4] end of the
+                                 attention (its last kernel).  They ride on the kernels'
+                                 own launches (hipExtLaunchKernel start / stop events),
+                                 so they add no marker packets to the stream; NULL =
+                                 none, and a NULL entry is not recorded.  With no block
+                                 to score, [0] and [1] are recorded as markers */
     int32_t release_previous; /* nonzero: before selecting, undo the recall of the
                                  previous pulse_decode_layer made with these buffers
                                  (table entries back to -1, free_head rewound; the hot
@@ -592,9 +595,12 @@ PULSE_API pulse_status pulse_probe_host_read(const void* host_src, void* dev_dst
  * device memory at `src` and folds them into one word per workgroup in
  * `sink` (device, pulse_probe_hbm_sink_bytes() bytes).  Timed over the byte
  * count of an HBM-bound kernel, it measures the read bandwidth the GPU
- * sustains at that size.
+ * sustains at that size.  start_event / stop_event (optional hipEvent_t):
+ * recorded at the kernel's start and end by its launch, as the layer-step's
+ * stage events are, so both are timed the same way.
  */
-PULSE_API pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, pulse_stream_t stream);
+PULSE_API pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, void* start_event,
+                                            void* stop_event, pulse_stream_t stream);
 PULSE_API size_t pulse_probe_hbm_sink_bytes(void);
 
 /* Timing events for pulse_layer_args.events: n hipEvent_t handles written to

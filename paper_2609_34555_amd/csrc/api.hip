@@ -356,15 +356,14 @@ namespace pulse {
 // The three stages of a chained layer-step (arguments already validated).
 // Score + select + recall plan; `mid` (optional) is recorded between score
 // and select.
-hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mid) {
+hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t score_start, hipEvent_t score_stop) {
     const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
     const ReleaseArgs rel{at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt), a.B, a.k_max,
                           a.block_table, a.max_blocks, a.free_head, a.stats, a.dev_status};
     hipError_t e = launch_score(a.shape, a.q, a.digests, a.blk_off, a.B, a.total_blocks, a.solo_kv_head,
                                 a.n_sink_blocks, a.n_local_blocks, at<float>(a.ws, w.scores), 1, hs,
-                                a.release_previous ? &rel : nullptr);
+                                a.release_previous ? &rel : nullptr, score_start, score_stop);
     if (e != hipSuccess) return e;
-    if (mid && (e = hipEventRecord(mid, hs)) != hipSuccess) return e;
     return launch_select(a.blk_off, a.B, a.total_blocks, at<float>(a.ws, w.scores), a.k_mid, a.n_sink_blocks,
                          a.n_local_blocks, a.k_max, a.sel_idx, a.sel_cnt, a.block_table, a.max_blocks, a.n_slots,
                          a.free_head, at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt),
@@ -373,21 +372,22 @@ hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mi
 }
 
 // Gather-scatter recall of the plan written by layer_select.
-hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs, int32_t copy_xcds) {
+hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs, int32_t copy_xcds, hipEvent_t start,
+                        hipEvent_t stop) {
     const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
     return launch_recall_copy(a.host_kv, a.blk_off, a.B, a.k_max, a.block_table, a.max_blocks, a.free_slots,
                               a.free_head, a.n_free, a.slot_pool, a.n_slots, pulse_block_bytes(&a.shape),
                               at<int32_t>(a.ws, w.miss_list), at<int32_t>(a.ws, w.miss_cnt),
                               at<int32_t>(a.ws, w.run_cnt), at<int32_t>(a.ws, w.req_err), at<int32_t>(a.ws, w.misc),
-                              a.stats, a.dev_status, copy_xcds, hs);
+                              a.stats, a.dev_status, copy_xcds, hs, start, stop);
 }
 
 // Sparse attention over the selection.
-hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs) {
+hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs, hipEvent_t done) {
     const WsLayout w = ws_layout(a.shape, a.B, a.k_max, a.total_blocks);
     return launch_attention(a.shape, a.q, a.slot_pool, a.n_slots, a.block_table, a.max_blocks, a.sel_idx, a.sel_cnt,
                             a.k_max, a.ctx_len, a.B, a.sm_scale, a.out, a.lse, at<float>(a.ws, w.attn_o),
-                            at<float2>(a.ws, w.attn_ml), a.dev_status, hs, (hipEvent_t)a.attn_split_event);
+                            at<float2>(a.ws, w.attn_ml), a.dev_status, hs, (hipEvent_t)a.attn_split_event, done);
 }
 
 // Full argument check of a chained layer-step.
@@ -416,22 +416,20 @@ pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream
     pulse_status st = check_layer_args(a);
     if (st != PULSE_OK || a->B == 0) return st;
     hipStream_t hs = (hipStream_t)stream;
+    // the timing events ride on the kernels' own launches (no marker packets); NULL entries are not recorded
     hipEvent_t* ev = (hipEvent_t*)a->events;
-    // each record costs a few microseconds on the stream, so absent (NULL) entries are skipped
-    auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], hs) == hipSuccess; };
-    if (!mark(0)) return PULSE_ERR_HIP;
-    if (layer_select(*a, hs, ev ? ev[1] : nullptr) != hipSuccess) return PULSE_ERR_HIP;
-    if (!mark(2)) return PULSE_ERR_HIP;
-    if (layer_recall(*a, hs) != hipSuccess) return PULSE_ERR_HIP;
-    if (!mark(3)) return PULSE_ERR_HIP;
-    if (layer_attention(*a, hs) != hipSuccess) return PULSE_ERR_HIP;
-    if (!mark(4)) return PULSE_ERR_HIP;
+    auto E = [&](int i) { return ev ? ev[i] : nullptr; };
+    if (layer_select(*a, hs, E(0), E(1)) != hipSuccess) return PULSE_ERR_HIP;
+    if (layer_recall(*a, hs, 8, E(2), E(3)) != hipSuccess) return PULSE_ERR_HIP;
+    if (layer_attention(*a, hs, E(4)) != hipSuccess) return PULSE_ERR_HIP;
     return PULSE_OK;
 }
 
-pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, pulse_stream_t stream) {
+pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, void* start_event, void* stop_event,
+                                  pulse_stream_t stream) {
     PULSE_REQUIRE(bytes % 16 == 0 && (src || bytes == 0) && sink, PULSE_ERR_INVALID_ARG);
-    return hip_status(launch_probe_hbm_read(src, bytes, (uint32_t*)sink, (hipStream_t)stream));
+    return hip_status(launch_probe_hbm_read(src, bytes, (uint32_t*)sink, (hipStream_t)stream,
+                                            (hipEvent_t)start_event, (hipEvent_t)stop_event));
 }
 
 size_t pulse_probe_hbm_sink_bytes(void) { return sizeof(uint32_t) * (size_t)probe_hbm_sink_words(); }

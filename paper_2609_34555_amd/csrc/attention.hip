@@ -27,8 +27,6 @@
 // per output element, with independent loads.  (Merging in the last workgroup
 // to finish would need a device-scope release fence per workgroup, which on
 // gfx950 writes back the XCD's L2 and costs more than the extra launch.)
-#include <hip/hip_ext.h>
-
 #include "pulse_internal.h"
 
 namespace pulse {
@@ -390,29 +388,23 @@ AttnPlan attn_plan(int32_t B, int32_t Hkv, int32_t k_max, int32_t bs) {
     return p;
 }
 
-// With `done`, the launch carries it as the kernel's stop event (recorded by the
-// dispatch itself at the kernel's completion, so timing it adds no marker packet).
+// `done` (optional): the kernel's stop event, carried by the launch.
 template <int DT, int BS, int W>
 static void launch_attn_t(dim3 grid, size_t lds, hipStream_t st, hipEvent_t done, const void* q, const void* pool,
                           int32_t n_slots, const int32_t* table, int32_t max_blocks, const int32_t* sel_idx,
                           const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t Hq, int32_t Hkv,
                           int32_t G, int32_t eps, int32_t n_wg, float scale_log2, float* ws_o, float2* ws_ml,
                           float* out, float* lse, int32_t* status) {
-    if (done)
-        hipExtLaunchKernelGGL(attn_splitk_kernel<DT, BS, W>, grid, dim3(W * kWave), (uint32_t)lds, st, nullptr, done,
-                              0u, (const uint16_t*)q, (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx,
-                              sel_cnt, k_max, ctx_len, Hq, Hkv, G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse,
-                              status);
-    else
-        hipLaunchKernelGGL((attn_splitk_kernel<DT, BS, W>), grid, dim3(W * kWave), lds, st, (const uint16_t*)q,
-                           (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max, ctx_len, Hq,
-                           Hkv, G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse, status);
+    launch_timed(attn_splitk_kernel<DT, BS, W>, grid, dim3(W * kWave), (uint32_t)lds, st, nullptr, done,
+                 (const uint16_t*)q, (const uint16_t*)pool, n_slots, table, max_blocks, sel_idx, sel_cnt, k_max,
+                 ctx_len, Hq, Hkv, G, eps, n_wg, scale_log2, ws_o, ws_ml, out, lse, status);
 }
 
 hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
                             const int32_t* table, int32_t max_blocks, const int32_t* sel_idx, const int32_t* sel_cnt,
                             int32_t k_max, const int32_t* ctx_len, int32_t B, float sm_scale, float* out, float* lse,
-                            float* ws_o, float2* ws_ml, int32_t* status, hipStream_t st, hipEvent_t split_done) {
+                            float* ws_o, float2* ws_ml, int32_t* status, hipStream_t st, hipEvent_t split_done,
+                            hipEvent_t done) {
     if (B == 0) return hipSuccess;
     const int32_t Hkv = s.num_kv_heads, Hq = s.num_q_heads, G = Hq / Hkv;
     const AttnPlan p = attn_plan(B, Hkv, k_max, s.block_size);
@@ -421,8 +413,10 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
     dim3 grid((unsigned)n_wg, (unsigned)Hkv, (unsigned)B);
     const size_t lds = sizeof(float) * W * G * kHeadDim + sizeof(float2) * W * G;
     const float scale_log2 = sm_scale * 1.4426950408889634f;
+    // stop event of the split-K kernel: split_done, or `done` when no combine follows it
+    const hipEvent_t splitk_stop = split_done ? split_done : (n_wg <= 1 ? done : nullptr);
 #define PULSE_ATTN(DT, BS, W)                                                                                        \
-    launch_attn_t<DT, BS, W>(grid, lds, st, split_done, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt,      \
+    launch_attn_t<DT, BS, W>(grid, lds, st, splitk_stop, q, pool, n_slots, table, max_blocks, sel_idx, sel_cnt,     \
                              k_max, ctx_len,                                                                        \
                              Hq, Hkv, G, p.entries_per_split, n_wg, scale_log2, ws_o, ws_ml, out, lse, status)
 #define PULSE_ATTN_W(DT, BS) \
@@ -439,9 +433,11 @@ hipError_t launch_attention(const pulse_shape& s, const void* q, const void* poo
 #undef PULSE_ATTN_W
 #undef PULSE_ATTN
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || n_wg <= 1) return e;
-    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)G, (unsigned)Hkv, (unsigned)B), dim3(kCombineThreads), 0,
-                       st, ws_o, ws_ml, sel_cnt, k_max, Hq, Hkv, G, p.entries_per_split, n_wg, W, out, lse);
+    if (e != hipSuccess) return e;
+    if (n_wg <= 1) return (done && split_done) ? hipEventRecord(done, st) : hipSuccess;
+    launch_timed(attn_combine_kernel, dim3((unsigned)G, (unsigned)Hkv, (unsigned)B), dim3(kCombineThreads), 0u, st,
+                 nullptr, done, (const float*)ws_o, (const float2*)ws_ml, sel_cnt, k_max, Hq, Hkv, G,
+                 p.entries_per_split, n_wg, W, out, lse);
     return hipGetLastError();
 }
 

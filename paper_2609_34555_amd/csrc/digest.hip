@@ -220,29 +220,31 @@ hipError_t launch_build_digests(const pulse_shape& s, const void* kv, const int6
 }
 
 template <int DT, int G>
-static void launch_score_t(int32_t heads, hipStream_t st, const void* q, const void* digests, const int64_t* blk_off,
-                           int32_t B, int64_t total, int32_t Hq, int32_t solo, int32_t n_sink, int32_t n_local,
-                           float* scores, const ReleaseArgs* rel) {
-    const size_t lds = sizeof(int64_t) * ((size_t)B + 1);
+static void launch_score_t(int32_t heads, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, const void* q,
+                           const void* digests, const int64_t* blk_off, int32_t B, int64_t total, int32_t Hq,
+                           int32_t solo, int32_t n_sink, int32_t n_local, float* scores, const ReleaseArgs* rel) {
+    const uint32_t lds = (uint32_t)(sizeof(int64_t) * ((size_t)B + 1));
     const ReleaseArgs ra = rel ? *rel : ReleaseArgs{};
     const int32_t dr = rel != nullptr;
     if (total * heads > kScoreLargeBlocks) {
         const dim3 grid((unsigned)((total + 31) / 32), (unsigned)heads);
-        hipLaunchKernelGGL((score_kernel<DT, G, 2, true>), grid, dim3(256), lds, st, (const uint16_t*)q,
-                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, ra, dr);
+        launch_timed(score_kernel<DT, G, 2, true>, grid, dim3(256), lds, st, ev0, ev1, (const uint16_t*)q,
+                     (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, ra, dr);
     } else {
         const dim3 grid((unsigned)((total + 15) / 16), (unsigned)heads);
-        hipLaunchKernelGGL((score_kernel<DT, G, 1, false>), grid, dim3(256), lds, st, (const uint16_t*)q,
-                           (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, ra, dr);
+        launch_timed(score_kernel<DT, G, 1, false>, grid, dim3(256), lds, st, ev0, ev1, (const uint16_t*)q,
+                     (const uint16_t*)digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, ra, dr);
     }
 }
 
 template <int DT>
-static void launch_score_dt(int G, int32_t heads, hipStream_t st, const void* q, const void* digests,
-                            const int64_t* blk_off, int32_t B, int64_t total, int32_t Hq, int32_t solo,
-                            int32_t n_sink, int32_t n_local, float* scores, const ReleaseArgs* rel) {
-#define PULSE_SCORE_CASE(g) \
-    case g: launch_score_t<DT, g>(heads, st, q, digests, blk_off, B, total, Hq, solo, n_sink, n_local, scores, rel); \
+static void launch_score_dt(int G, int32_t heads, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1, const void* q,
+                            const void* digests, const int64_t* blk_off, int32_t B, int64_t total, int32_t Hq,
+                            int32_t solo, int32_t n_sink, int32_t n_local, float* scores, const ReleaseArgs* rel) {
+#define PULSE_SCORE_CASE(g)                                                                                    \
+    case g:                                                                                                    \
+        launch_score_t<DT, g>(heads, st, ev0, ev1, q, digests, blk_off, B, total, Hq, solo, n_sink, n_local,  \
+                              scores, rel);                                                                    \
         break;
     switch (G) {
         PULSE_SCORE_CASE(1) PULSE_SCORE_CASE(2) PULSE_SCORE_CASE(3) PULSE_SCORE_CASE(4)
@@ -256,15 +258,20 @@ static void launch_score_dt(int G, int32_t heads, hipStream_t st, const void* q,
 
 hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
                         int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
-                        float* scores, int32_t heads, hipStream_t st, const ReleaseArgs* rel) {
-    if (total_blocks == 0) return hipSuccess;  // no blocks: no recall to release either
+                        float* scores, int32_t heads, hipStream_t st, const ReleaseArgs* rel, hipEvent_t start,
+                        hipEvent_t stop) {
+    if (total_blocks == 0) {  // no blocks: no recall to release either; requested events become markers
+        hipError_t e = start ? hipEventRecord(start, st) : hipSuccess;
+        if (e == hipSuccess && stop) e = hipEventRecord(stop, st);
+        return e;
+    }
     const int G = s.num_q_heads / s.num_kv_heads;
     if (s.dtype == PULSE_BF16)
-        launch_score_dt<PULSE_BF16>(G, heads, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
-                                    n_local, scores, rel);
+        launch_score_dt<PULSE_BF16>(G, heads, st, start, stop, q, digests, blk_off, B, total_blocks, s.num_q_heads,
+                                    solo, n_sink, n_local, scores, rel);
     else
-        launch_score_dt<PULSE_F16>(G, heads, st, q, digests, blk_off, B, total_blocks, s.num_q_heads, solo, n_sink,
-                                   n_local, scores, rel);
+        launch_score_dt<PULSE_F16>(G, heads, st, start, stop, q, digests, blk_off, B, total_blocks, s.num_q_heads,
+                                   solo, n_sink, n_local, scores, rel);
     return hipGetLastError();
 }
 

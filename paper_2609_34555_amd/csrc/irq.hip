@@ -238,7 +238,7 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
         if (!ev_sel[m] || !ev_rc0[m] || !ev_rc1[m] || !ev_att[m]) { result = PULSE_ERR_HIP; break; }
         // selection on the compute stream, then the recall: the GPU gather kernel + signal on
         // the I/O stream, or a submission to the gather-scatter engine
-        if (layer_select(a, irq->cmp, nullptr) != hipSuccess || hipEventRecord(ev_sel[m], irq->cmp) != hipSuccess) {
+        if (layer_select(a, irq->cmp) != hipSuccess || hipEventRecord(ev_sel[m], irq->cmp) != hipSuccess) {
             result = PULSE_ERR_HIP;
             break;
         }

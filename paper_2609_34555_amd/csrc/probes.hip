@@ -43,13 +43,15 @@ __global__ __launch_bounds__(kProbeThreads) void probe_hbm_read_kernel(const u32
 
 int32_t probe_hbm_sink_words() { return kProbeGrid; }
 
-hipError_t launch_probe_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st) {
+hipError_t launch_probe_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st, hipEvent_t start,
+                                 hipEvent_t stop) {
     const int64_t n16 = (int64_t)(bytes / 16);
     if (n16 == 0) return hipSuccess;
     // enough workgroups for four loads in flight per thread, at most kProbeGrid
     const int64_t need = (n16 + 4 * kProbeThreads - 1) / (4 * kProbeThreads);
     const unsigned grid = (unsigned)(need < 1 ? 1 : (need < kProbeGrid ? need : kProbeGrid));
-    hipLaunchKernelGGL(probe_hbm_read_kernel, dim3(grid), dim3(kProbeThreads), 0, st, (const u32x4*)src, n16, sink);
+    launch_timed(probe_hbm_read_kernel, dim3(grid), dim3(kProbeThreads), 0u, st, start, stop, (const u32x4*)src, n16,
+                 sink);
     return hipGetLastError();
 }
 

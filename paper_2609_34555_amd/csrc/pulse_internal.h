@@ -2,6 +2,7 @@
 // declarations shared by the gfx950 kernels of the sparse-KV decode path.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -22,6 +23,20 @@ constexpr int kHeadDim = 128;
 constexpr int kWave = 64;
 constexpr int kMaxGroup = 16;   // G = Hq / Hkv padded to one 16-wide MFMA tile
 constexpr int kChunkTokens = 32;  // attention processes 32 tokens per MFMA step
+
+// ---- timed launches ---------------------------------------------------------
+
+// Launch with optional timing events carried by the dispatch itself
+// (hipExtLaunchKernel: `start` is recorded when the kernel starts, `stop` when it
+// completes), so timing a kernel adds no marker packet to the stream.
+template <typename F, typename... Args>
+inline void launch_timed(F kernel, dim3 grid, dim3 block, uint32_t lds, hipStream_t st, hipEvent_t start,
+                         hipEvent_t stop, Args... args) {
+    if (start || stop)
+        hipExtLaunchKernelGGL(kernel, grid, block, lds, st, start, stop, 0u, args...);
+    else
+        hipLaunchKernelGGL(kernel, grid, block, lds, st, args...);
+}
 
 // ---- device status --------------------------------------------------------
 
@@ -164,9 +179,12 @@ __device__ inline void release_entries(const ReleaseArgs& a, int64_t e0, int64_t
 // rel != nullptr: the scoring kernel also releases the recall described by rel
 // (every entry's table reset, then the free-list head and statistics), which
 // the kernel boundary orders before the selection that follows.
+// start / stop (optional): timing events of the scoring kernel (recorded as
+// markers when there is no block to score).
 hipError_t launch_score(const pulse_shape& s, const void* q, const void* digests, const int64_t* blk_off,
                         int32_t B, int64_t total_blocks, int32_t solo, int32_t n_sink, int32_t n_local,
-                        float* scores, int32_t heads, hipStream_t st, const ReleaseArgs* rel = nullptr);
+                        float* scores, int32_t heads, hipStream_t st, const ReleaseArgs* rel = nullptr,
+                        hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 // select (a3); when table != nullptr the set difference (a4) is folded in and
 // the recall plan (miss list, counts, runs, free_head snapshot) is written.
@@ -188,13 +206,15 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
                               int32_t* free_head, int32_t n_free, void* pool, int32_t n_slots,
                               size_t unit_bytes, const int32_t* miss_list, const int32_t* miss_cnt,
                               const int32_t* run_cnt, const int32_t* req_err, const int32_t* misc,
-                              pulse_recall_stats* stats, int32_t* status, int32_t copy_xcds, hipStream_t st);
+                              pulse_recall_stats* stats, int32_t* status, int32_t copy_xcds, hipStream_t st,
+                              hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 
 hipError_t launch_attention(const pulse_shape& s, const void* q, const void* pool, int32_t n_slots,
                             const int32_t* table, int32_t max_blocks, const int32_t* sel_idx,
                             const int32_t* sel_cnt, int32_t k_max, const int32_t* ctx_len, int32_t B,
                             float sm_scale, float* out, float* lse, float* ws_o, float2* ws_ml,
-                            int32_t* status, hipStream_t st, hipEvent_t split_done = nullptr);
+                            int32_t* status, hipStream_t st, hipEvent_t split_done = nullptr,
+                            hipEvent_t done = nullptr);
 
 hipError_t launch_average_scores(const float* sc, int64_t total_blocks, int32_t H, float* avg, hipStream_t st);
 hipError_t launch_mam_selection(const int32_t* ctx_len, int32_t B, int32_t bs, int32_t max_blocks, int32_t n_sink,
@@ -217,15 +237,20 @@ inline T* ws_at(void* ws, size_t off) {
 
 // Stages of a chained layer-step (api.hip): score + select + plan, recall,
 // attention; and the full argument check of pulse_layer_args.
-hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t mid);
-hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs, int32_t copy_xcds = 8);
-hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs);
+// Optional timing events (NULL = none): the scoring kernel's start / end, the
+// recall copy kernel's start / end, the end of the attention's last kernel.
+hipError_t layer_select(const pulse_layer_args& a, hipStream_t hs, hipEvent_t score_start = nullptr,
+                        hipEvent_t score_stop = nullptr);
+hipError_t layer_recall(const pulse_layer_args& a, hipStream_t hs, int32_t copy_xcds = 8,
+                        hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
+hipError_t layer_attention(const pulse_layer_args& a, hipStream_t hs, hipEvent_t done = nullptr);
 pulse_status check_layer_args(const pulse_layer_args* a);
 
 hipError_t launch_release(const int32_t* miss_list, const int32_t* miss_cnt, int32_t B, int32_t k_max,
                           int32_t* table, int32_t max_blocks, int32_t* free_head, pulse_recall_stats* stats,
                           int32_t* status, hipStream_t st);
-hipError_t launch_probe_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st);
+hipError_t launch_probe_hbm_read(const void* src, size_t bytes, uint32_t* sink, hipStream_t st,
+                                 hipEvent_t start = nullptr, hipEvent_t stop = nullptr);
 int32_t probe_hbm_sink_words();
 
 hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st);

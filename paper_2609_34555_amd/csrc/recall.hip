@@ -270,7 +270,7 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
                               void* pool, int32_t n_slots, size_t unit_bytes, const int32_t* miss_list,
                               const int32_t* miss_cnt, const int32_t* run_cnt, const int32_t* req_err,
                               const int32_t* misc, pulse_recall_stats* stats, int32_t* status, int32_t copy_xcds,
-                              hipStream_t st) {
+                              hipStream_t st, hipEvent_t start, hipEvent_t stop) {
     if (B == 0) return hipSuccess;
     // 16-byte loads in flight per thread: the largest of PULSE_RECALL_LPT, 4, 2 whose
     // 4 KiB * LPT chunk divides the block
@@ -280,10 +280,10 @@ hipError_t launch_recall_copy(const void* host_kv, const int64_t* blk_off, int32
     const int64_t chunk = 4096 * (int64_t)lpt;
     const int64_t max_chunks = (int64_t)B * k_max * (int64_t)(unit_bytes / chunk);
     const unsigned grid = (unsigned)(max_chunks < kRecallGrid ? (max_chunks > 0 ? max_chunks : 1) : kRecallGrid);
-#define PULSE_COPY(L)                                                                                            \
-    hipLaunchKernelGGL(recall_copy_kernel<L>, dim3(grid), dim3(kCopyThreads), 0, st, (const uint8_t*)host_kv,    \
-                       blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool, n_slots, \
-                       (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status, copy_xcds)
+#define PULSE_COPY(L)                                                                                              \
+    launch_timed(recall_copy_kernel<L>, dim3(grid), dim3(kCopyThreads), 0u, st, start, stop, (const uint8_t*)host_kv, \
+                 blk_off, B, k_max, table, max_blocks, free_slots, free_head, n_free, (uint8_t*)pool, n_slots,        \
+                 (int64_t)unit_bytes, miss_list, miss_cnt, run_cnt, req_err, misc, stats, status, copy_xcds)
     if (lpt == 8) PULSE_COPY(8);
     else if (lpt == 4) PULSE_COPY(4);
     else PULSE_COPY(2);

@@ -134,7 +134,7 @@ def lib():
             "pulse_host_free": (ctypes.c_int, [_P]),
             "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
             "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
-            "pulse_probe_hbm_read": (ctypes.c_int, [_P, SZ, _P, _P]),
+            "pulse_probe_hbm_read": (ctypes.c_int, [_P, SZ, _P, _P, _P, _P]),
             "pulse_release_recalled": (ctypes.c_int, [SP, I32, I32, I64, _P, I32, _P, _P, _P, _P, SZ, _P]),
             "pulse_probe_hbm_sink_bytes": (SZ, []),
             "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
@@ -382,8 +382,8 @@ def pulse_probe_host_read(host_src, dev_dst, nbytes, stream=None, check=True):
     return _check(st, "pulse_probe_host_read", check)
 
 
-def pulse_probe_hbm_read(src, nbytes, sink, stream=None, check=True):
-    st = lib().pulse_probe_hbm_read(_ptr(src), nbytes, _ptr(sink), _stream(stream))
+def pulse_probe_hbm_read(src, nbytes, sink, stream=None, check=True, start_event=None, stop_event=None):
+    st = lib().pulse_probe_hbm_read(_ptr(src), nbytes, _ptr(sink), start_event, stop_event, _stream(stream))
     return _check(st, "pulse_probe_hbm_read", check)
 
 
