@@ -98,7 +98,7 @@ static pulse_status check_select_args(const pulse_shape* shape, const void* q, c
     PULSE_REQUIRE(B >= 0 && total_blocks >= 0 && k_max >= 1, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(n_sink >= 0 && n_local >= 0, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(solo >= 0 && solo < shape->num_kv_heads, PULSE_ERR_INVALID_ARG);
-    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
+    PULSE_REQUIRE(B <= kMaxBatch, PULSE_ERR_UNSUPPORTED);
     if (B == 0) return PULSE_OK;
     PULSE_REQUIRE(q && blk_off && k_mid && sel_idx && sel_cnt && dev_status, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(digests || total_blocks == 0, PULSE_ERR_INVALID_ARG);
@@ -228,7 +228,7 @@ pulse_status pulse_mam(const pulse_shape* shape, const void* q, const void* slot
     PULSE_REQUIRE(shape_supported(shape), PULSE_ERR_UNSUPPORTED);
     PULSE_REQUIRE(B >= 0 && max_blocks >= 1 && n_slots >= 1 && n_sink_blocks >= 0 && n_local_blocks >= 0,
                   PULSE_ERR_INVALID_ARG);
-    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
+    PULSE_REQUIRE(B <= kMaxBatch, PULSE_ERR_UNSUPPORTED);
     if (B == 0) return PULSE_OK;
     PULSE_REQUIRE(q && slot_pool && block_table && ctx_len && mam && dev_status, PULSE_ERR_INVALID_ARG);
     const MamLayout m = mam_layout(*shape, B, max_blocks);
@@ -281,7 +281,7 @@ static pulse_status check_recall_args(const pulse_shape* shape, const void* host
     PULSE_REQUIRE(shape_supported(shape), PULSE_ERR_UNSUPPORTED);
     PULSE_REQUIRE(B >= 0 && k_max >= 1 && max_blocks >= 1 && n_free >= 0 && n_slots >= 1,
                   PULSE_ERR_INVALID_ARG);
-    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
+    PULSE_REQUIRE(B <= kMaxBatch, PULSE_ERR_UNSUPPORTED);
     if (B == 0) return PULSE_OK;
     PULSE_REQUIRE(host_kv && blk_off && sel_idx && sel_cnt && block_table && free_head && slot_pool && stats &&
                       dev_status,
@@ -322,7 +322,7 @@ pulse_status pulse_release_recalled(const pulse_shape* shape, int32_t B, int32_t
     PULSE_REQUIRE(shape, PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(shape_supported(shape), PULSE_ERR_UNSUPPORTED);
     PULSE_REQUIRE(B >= 0 && k_max >= 1 && max_blocks >= 1 && total_blocks >= 0, PULSE_ERR_INVALID_ARG);
-    PULSE_REQUIRE(B <= 4096, PULSE_ERR_UNSUPPORTED);
+    PULSE_REQUIRE(B <= kMaxBatch, PULSE_ERR_UNSUPPORTED);
     if (B == 0) return PULSE_OK;
     PULSE_REQUIRE(block_table && free_head && stats && dev_status, PULSE_ERR_INVALID_ARG);
     const WsLayout w = ws_layout(*shape, B, k_max, total_blocks);

@@ -54,12 +54,12 @@ __global__ __launch_bounds__(kPublishThreads) void publish_plan_kernel(
     const int32_t* __restrict__ run_cnt, const int32_t* __restrict__ req_err, const int32_t* __restrict__ misc,
     pulse_recall_stats* __restrict__ stats, int32_t* status, Mailbox* mb, int64_t* mb_src, int32_t* mb_slot,
     int64_t cap, int64_t seq) {
-    __shared__ int32_t off[4097];
+    __shared__ int32_t off[kMaxBatch + 1];
     __shared__ uint32_t sh_runs, sh_bad, sh_slot_bad;
     const int tid = threadIdx.x;
     if (tid == 0) {
         uint32_t acc = 0, runs = 0, bad = 0;
-        for (int i = 0; i < B; ++i) {  // B <= 4096, one thread: small
+        for (int i = 0; i < B; ++i) {  // B <= kMaxBatch, one thread: small
             off[i] = (int32_t)acc;
             acc += (uint32_t)miss_cnt[i];
             runs += (uint32_t)run_cnt[i];
@@ -392,7 +392,7 @@ pulse_status pulse_gs_recall_submit(pulse_gs_engine* e, const void* host_kv, con
     if (!e || !seq_out) return PULSE_ERR_INVALID_ARG;
     *seq_out = 0;
     if (B < 0 || k_max < 1 || max_blocks < 1 || n_free < 0 || n_slots < 1) return PULSE_ERR_INVALID_ARG;
-    if (B > 4096) return PULSE_ERR_UNSUPPORTED;
+    if (B > kMaxBatch) return PULSE_ERR_UNSUPPORTED;
     if (B == 0) return PULSE_OK;
     if (!host_kv || !blk_off || !sel_idx || !sel_cnt || !block_table || !free_head || !slot_pool || !stats ||
         !dev_status || (!free_slots && n_free))

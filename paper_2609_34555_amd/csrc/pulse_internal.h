@@ -23,6 +23,7 @@ constexpr int kHeadDim = 128;
 constexpr int kWave = 64;
 constexpr int kMaxGroup = 16;   // G = Hq / Hkv padded to one 16-wide MFMA tile
 constexpr int kChunkTokens = 32;  // attention processes 32 tokens per MFMA step
+constexpr int kMaxBatch = 4096;   // requests per call: the recall and publish kernels scan their counts in LDS
 
 // ---- timed launches ---------------------------------------------------------
 

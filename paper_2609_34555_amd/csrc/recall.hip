@@ -38,7 +38,6 @@ constexpr int64_t kRecallGrid = PULSE_RECALL_GRID;  // persistent copy workgroup
 // XCD's 16 workgroups still reach the link rate, and the other XCDs stay free for
 // concurrent kernels (which then also take a little link bandwidth); with 8, all do.
 constexpr int kXcds = 8;
-constexpr int kMaxBatch = 4096;  // requests per call supported by the copy kernel
 
 __device__ inline uint64_t lanemask_lt_r() {
     const int lane = threadIdx.x & 63;
