@@ -388,7 +388,10 @@ typedef struct {
                                  own launches (hipExtLaunchKernel start / stop events),
                                  so they add no marker packets to the stream; NULL =
                                  none, and a NULL entry is not recorded.  With no block
-                                 to score, [0] and [1] are recorded as markers */
+                                 to score, [0] and [1] are recorded as markers.  A step
+                                 captured into a HIP graph is captured without them
+                                 (events and attn_split_event NULL; that is the form
+                                 whose replays are tested) */
     int32_t release_previous; /* nonzero: before selecting, undo the recall of the
                                  previous pulse_decode_layer made with these buffers
                                  (table entries back to -1, free_head rewound; the hot
