@@ -80,8 +80,10 @@ typedef struct {
 
 /* Device-resident statistics written by the recall (device memory). */
 typedef struct {
-    int32_t n_missing; /* blocks recalled (on pool exhaustion: blocks that would be) */
-    int32_t n_runs;    /* maximal runs of consecutive missing block indices */
+    int32_t n_missing; /* blocks recalled (on pool exhaustion or a bad free slot: blocks
+                          that would be; on a malformed selection: 0) */
+    int32_t n_runs;    /* maximal runs of consecutive missing block indices (0 on a
+                          malformed selection) */
     int64_t bytes;     /* bytes copied host -> slot pool (0 on any device error) */
 } pulse_recall_stats;
 
@@ -274,7 +276,11 @@ PULSE_API pulse_status pulse_pick_solo_heads(const float* mam, int32_t rows, int
  *   dev_status   device int32, required
  * If #missing > n_free - *free_head, PULSE_ERR_POOL_EXHAUSTED is reported and
  * the table, pool and free_head are left unchanged; likewise for any index
- * outside its buffer (PULSE_ERR_BAD_INDEX).
+ * outside its buffer (PULSE_ERR_BAD_INDEX): a selection entry, a block_table
+ * entry >= n_slots, *free_head outside [0, n_free], or any of the slots
+ * free_slots[*free_head .. *free_head + #missing) outside [0, n_slots).  Every
+ * slot is checked before anything is written, so on any of these errors no
+ * table entry, pool byte or free_head changes and stats.bytes is 0.
  */
 PULSE_API pulse_status pulse_recall_gather(const pulse_shape* shape, const void* host_kv, const int64_t* blk_off,
                                  int32_t B, const int32_t* sel_idx, const int32_t* sel_cnt, int32_t k_max,

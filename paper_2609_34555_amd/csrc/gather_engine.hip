@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kPublishThreads) void publish_plan_kernel(
     pulse_recall_stats* __restrict__ stats, int32_t* status, Mailbox* mb, int64_t* mb_src, int32_t* mb_slot,
     int64_t cap, int64_t seq) {
     __shared__ int32_t off[kMaxBatch + 1];
-    __shared__ uint32_t sh_runs, sh_bad, sh_slot_bad;
+    __shared__ uint32_t sh_runs, sh_bad;
     const int tid = threadIdx.x;
     if (tid == 0) {
         uint32_t acc = 0, runs = 0, bad = 0;
@@ -68,15 +68,22 @@ __global__ __launch_bounds__(kPublishThreads) void publish_plan_kernel(
         off[B] = (int32_t)acc;
         sh_runs = runs;
         sh_bad = bad;
-        sh_slot_bad = 0;
     }
     __syncthreads();
     const int64_t total = off[B];
     const int32_t fh0 = misc[0];
     const bool ok = sh_bad == 0;
-    const bool fits = fh0 >= 0 && fh0 <= n_free && total <= (int64_t)n_free - fh0;
+    const bool head_ok = fh0 >= 0 && fh0 <= n_free;
+    const bool fits = head_ok && total <= (int64_t)n_free - fh0;
     const bool room = total <= cap;
-    const bool go = ok && fits && room;
+    // First pass: every slot the recall takes must lie inside the pool.  Nothing is
+    // written (table, free-list head, statistics, mailbox plan) unless all of them do.
+    int slot_bad = 0;
+    if (ok && fits && room)
+        for (int64_t g = tid; g < total; g += kPublishThreads)
+            slot_bad |= (uint32_t)free_slots[fh0 + g] >= (uint32_t)n_slots;
+    const bool any_slot_bad = __syncthreads_or(slot_bad) != 0;
+    const bool go = ok && fits && room && !any_slot_bad;
     if (go) {
         for (int64_t g = tid; g < total; g += kPublishThreads) {
             int lo = 0, hi = B;
@@ -86,12 +93,6 @@ __global__ __launch_bounds__(kPublishThreads) void publish_plan_kernel(
             }
             const int32_t j = miss_list[(size_t)lo * k_max + (g - off[lo])];
             const int32_t slot = free_slots[fh0 + g];
-            if (slot < 0 || slot >= n_slots) {
-                atomicOr(&sh_slot_bad, 1u);
-                mb_src[g] = -1;
-                mb_slot[g] = -1;
-                continue;
-            }
             table[(size_t)lo * max_blocks + j] = slot;
             mb_src[g] = blk_off[lo] + j;
             mb_slot[g] = slot;
@@ -101,14 +102,14 @@ __global__ __launch_bounds__(kPublishThreads) void publish_plan_kernel(
     __syncthreads();         // ... before thread 0 publishes the sequence number
     if (tid == 0) {
         int32_t err = 0;
-        if (!ok) err = PULSE_ERR_BAD_INDEX;
+        if (!ok || !head_ok) err = PULSE_ERR_BAD_INDEX;
         else if (!fits) err = PULSE_ERR_POOL_EXHAUSTED;
         else if (!room) err = PULSE_ERR_WORKSPACE;
-        else if (sh_slot_bad) err = PULSE_ERR_BAD_INDEX;
-        if (err && err != PULSE_ERR_BAD_INDEX) report(status, err);
-        if (sh_slot_bad) report(status, PULSE_ERR_BAD_INDEX);
-        stats->n_missing = (int32_t)total;
-        stats->n_runs = (int32_t)sh_runs;
+        else if (any_slot_bad) err = PULSE_ERR_BAD_INDEX;
+        if (err) report(status, err);
+        // a malformed selection (already reported by the plan) leaves no statistics
+        stats->n_missing = ok ? (int32_t)total : 0;
+        stats->n_runs = ok ? (int32_t)sh_runs : 0;
         stats->bytes = go ? total * U : 0;
         if (go) *free_head = fh0 + (int32_t)total;
         mb->n_blocks = go ? total : 0;

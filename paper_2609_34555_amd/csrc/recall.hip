@@ -180,15 +180,40 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
     __syncthreads();
     const int64_t total = off[B];
     const bool ok = sh_bad == 0;
-    const bool fits = fh0 >= 0 && fh0 <= n_free && total <= (int64_t)n_free - fh0;
-    if (blockIdx.x == 0 && tid == 0) {
-        stats->n_missing = (int32_t)total;
-        stats->n_runs = (int32_t)sh_runs;
-        stats->bytes = (ok && fits) ? total * U : 0;
-        if (ok && !fits) report(status, PULSE_ERR_POOL_EXHAUSTED);
-        if (ok && fits) *free_head = fh0 + (int32_t)total;
+    const bool head_ok = fh0 >= 0 && fh0 <= n_free;
+    const bool fits = head_ok && total <= (int64_t)n_free - fh0;
+    // Every slot the recall takes must lie inside the pool.  Each workgroup checks the
+    // whole range free_slots[fh0, fh0 + total) before anything is written, so either all
+    // workgroups copy or none does, and on a bad slot the table, free-list head, pool and
+    // byte count stay as they were.  kSlotCheckLoads independent loads per thread are in
+    // flight per pass (an L2-resident list of at most B * k_max entries).
+    int slot_bad = 0;
+    if (ok && fits) {
+        constexpr int kSlotCheckLoads = 8;
+        for (int64_t g0 = tid; g0 < total; g0 += (int64_t)kSlotCheckLoads * kCopyThreads) {
+            int32_t s[kSlotCheckLoads];
+#pragma unroll
+            for (int k = 0; k < kSlotCheckLoads; ++k) {
+                const int64_t g = g0 + (int64_t)k * kCopyThreads;
+                s[k] = g < total ? free_slots[fh0 + g] : 0;
+            }
+#pragma unroll
+            for (int k = 0; k < kSlotCheckLoads; ++k) slot_bad |= (uint32_t)s[k] >= (uint32_t)n_slots;
+        }
     }
-    if (!ok || !fits) return;
+    slot_bad = __syncthreads_or(slot_bad);
+    const bool go = ok && fits && !slot_bad;
+    if (blockIdx.x == 0 && tid == 0) {
+        // a malformed selection (already reported by the plan) leaves no statistics
+        stats->n_missing = ok ? (int32_t)total : 0;
+        stats->n_runs = ok ? (int32_t)sh_runs : 0;
+        stats->bytes = go ? total * U : 0;
+        if (ok && !head_ok) report(status, PULSE_ERR_BAD_INDEX);
+        else if (ok && !fits) report(status, PULSE_ERR_POOL_EXHAUSTED);
+        else if (ok && slot_bad) report(status, PULSE_ERR_BAD_INDEX);
+        if (go) *free_head = fh0 + (int32_t)total;
+    }
+    if (!go) return;
     constexpr int64_t chunk = 4096 * LPT;
     const int64_t cpb = U / chunk;
     const int64_t n_chunks = total * cpb;
@@ -213,10 +238,7 @@ __global__ __launch_bounds__(kCopyThreads) void recall_copy_kernel(
             const int r = lo;
             const int32_t j = miss_list[(size_t)r * k_max + (g - off[r])];
             const int32_t slot = free_slots[fh0 + g];
-            if (slot < 0 || slot >= n_slots) {
-                if (tid == 0 && part == 0) report(status, PULSE_ERR_BAD_INDEX);
-                continue;
-            }
+            if (slot < 0 || slot >= n_slots) continue;  // checked above; guards the store all the same
             const uint8_t* src = host + (blk_off[r] + j) * U + part * chunk;
             uint8_t* dst = pool + (int64_t)slot * U + part * chunk;
             copy_chunk<LPT, decltype(nt)::value>(src, dst, tid);

@@ -58,11 +58,14 @@ def assert_selection_ok(w, gidx, gcnt, oidx, ocnt, oscores):
     return n_ties
 
 
-def oracle_recall(w, idx, cnt):
+def oracle_recall(w, idx, cnt, free_slots=None, free_head=0):
+    """The oracle's recall of selection (idx, cnt) from the workload's initial table and pool;
+    free_slots / free_head default to the workload's free list and 0."""
     table = w.table0.copy()
     pool = W.initial_pool(w).view(np.uint8).reshape(w.n_slots, -1).copy()
     host = w.kv.view(np.uint8).reshape(w.total_blocks, -1)
-    rc, fh, stats = O.recall(host, w.blk_off, idx, cnt, table, w.free_slots, 0, pool, w.unit_bytes)
+    free = w.free_slots if free_slots is None else free_slots
+    rc, fh, stats = O.recall(host, w.blk_off, idx, cnt, table, free, free_head, pool, w.unit_bytes)
     return rc, table, pool, fh, stats
 
 

@@ -244,6 +244,87 @@ def test_recall_rejects_unsorted_and_out_of_range():
     st.recall()
     torch.cuda.synchronize()
     assert st.status() == P.PULSE_ERR_BAD_INDEX and torch.equal(st.table, st.table0)
+    gidx, gcnt = st.selection()
+    rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt)
+    assert rc == O.ERR_BAD_INDEX and stats == (0, 0, 0)
+    assert_recall_equal(st, table, pool, fh, stats)
+
+
+BAD_FREE = ["slot_past_pool", "negative_slot", "head_past_list", "bad_slot_past_range"]
+
+
+@pytest.mark.parametrize("bad", BAD_FREE)
+@pytest.mark.parametrize("path", ["recall_gather", "decode_layer", "engine"])
+def test_recall_rejects_bad_free_slot(path, bad):
+    """A free list whose entries in the range the recall takes lie outside the pool, or a
+    free-list head outside the list: BAD_INDEX, and table, free head, statistics and every
+    pool byte exactly as the oracle leaves them (nothing written, bytes 0).  A bad entry
+    past that range is never read.  Afterwards a clean recall on the same state matches the
+    oracle.  Covers the standalone recall, the chained layer-step and the paper's engine."""
+    spec, s = W.custom("badfree", [3000, 2000, 700], Hq=32, Hkv=8, bs=16, k_mid=40, n_sink=1, n_local=8,
+                       resident_frac=0.05, heavy_per_req=10)
+    w, st = build(spec, s)
+    eng = (P.GatherScatterEngine(st.shape, n_workers=2, max_blocks_per_call=w.B * st.k_max, staging_blocks=16)
+           if path == "engine" else None)
+    try:
+        st.select()
+        torch.cuda.synchronize()
+        gidx, gcnt = st.selection()
+        rc0, _, _, _, clean = oracle_recall(w, gidx, gcnt)
+        n_miss = clean[0]
+        assert rc0 == 0 and n_miss >= 3 and n_miss < w.free_slots.size
+        free, fh0 = w.free_slots.copy(), 0
+        if bad == "slot_past_pool":
+            free[n_miss - 1] = w.n_slots  # the last slot the recall takes
+        elif bad == "negative_slot":
+            free[n_miss // 2] = -3
+        elif bad == "head_past_list":
+            fh0 = int(w.free_slots.size) + 1
+        else:
+            free[n_miss] = -1  # first entry past the range: not read
+        st.reset()
+        st.free_slots.copy_(torch.from_numpy(free))
+        st.free_head.fill_(fh0)
+        pool0 = st.pool.clone()
+
+        def run():
+            if path == "recall_gather":
+                st.recall()
+            elif path == "decode_layer":
+                st.decode_layer()
+            else:
+                seq = st.recall_gs(eng, wait=False)
+                try:
+                    eng.wait(seq, 20000)
+                except P.PulseError as e:  # the call's device status
+                    assert e.status == P.PULSE_ERR_BAD_INDEX
+            torch.cuda.synchronize()
+
+        run()
+        gidx, gcnt = st.selection()
+        rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt, free_slots=free, free_head=fh0)
+        say(f"  {path}/{bad}: oracle rc={rc} stats={stats}; gpu status={st.status()} stats={st.recall_stats()}")
+        if bad == "bad_slot_past_range":
+            assert rc == 0 and st.status() == 0
+            assert_recall_equal(st, table, pool, fh, stats)
+            return
+        assert rc == O.ERR_BAD_INDEX and stats[2] == 0
+        assert st.status() == P.PULSE_ERR_BAD_INDEX
+        assert torch.equal(st.table, st.table0) and torch.equal(st.pool, pool0)
+        assert_recall_equal(st, table, pool, fh, stats)
+        # nothing changed: a clean recall of the same selection on this state matches the oracle
+        st.free_slots.copy_(torch.from_numpy(w.free_slots))
+        st.free_head.fill_(0)
+        st.dev_status.zero_()
+        run()
+        assert st.status() == 0
+        gidx, gcnt = st.selection()
+        rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt)
+        assert rc == 0 and stats == clean
+        assert_recall_equal(st, table, pool, fh, stats)
+    finally:
+        if eng is not None:
+            eng.destroy()
 
 
 # ------------------------------------------------------------------ attention
