@@ -1,13 +1,14 @@
 """Interruptible layer-wise scheduling (Sec. 4.2) on the GPU: every detection mode must
-leave the offload batch's results identical to the chained single-stream path, and the
-normal batch's layers must compute attention + SwiGLU FFN correctly."""
+leave the offload batch's results identical to the chained single-stream path and, layer by
+layer, equal to the CPU oracle (digests, selection, table, free head, statistics, pool bytes,
+attention); the normal batch's layers must compute attention + SwiGLU FFN correctly."""
 import pytest
 import torch
 
 from paper_2609_34555_amd import pulse as P
 from paper_2609_34555_amd.harness import MultiLayerStep, NormalBatch
 
-from parity import say
+from parity import full_check, say
 
 pytestmark = pytest.mark.gpu
 
@@ -63,6 +64,9 @@ def test_irq_mode_matches_chained(setup, mode, use_engine):
         assert torch.equal(st.table, t) and torch.equal(st.pool, p)
         assert st.recall_stats() == rs
     assert normal.status() == 0
+    for i, st in enumerate(ml.layers):  # every offload layer against the oracle, as the step left it
+        res = full_check(st.w, st, run=False)
+        say(f"  layer {i}: oracle stats={res['stats']} ties={res['ties']} attn_err={res['attn_err'][0]:.1e}")
     if mode == "blocking":
         assert stats["normal_layers"] == N_OFF and depth.sum() == 0
     else:
