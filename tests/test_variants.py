@@ -81,12 +81,24 @@ def test_average_selection_matches_oracle(name, kw):
     assert rc == 0
     gidx, gcnt = st.selection()
     n_ties = assert_selection_ok(w, gidx, gcnt, oidx, ocnt, avg)
-    # averaged scores of middle blocks, fp32 accumulation vs exact
-    g = scores.cpu().numpy()
+    # Averaged scores of middle blocks, fp32 against exact.  Each head's fp32 score carries the
+    # SoloHead scores' bound (4e-6 of max(|s_h|, 1), the d*G-term fp32 sum); the kernel then adds
+    # the Hkv head scores in fp32 (at most Hkv roundings of 2^-24 of the running sum of |s_h|)
+    # and scales by 1/Hkv.  So |avg_gpu - avg| <= mean_h 4e-6 max(|s_h|, 1) + Hkv 2^-24 mean_h |s_h|.
+    heads = np.stack([O.score(w.q, O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, h),
+                              w.blk_off, w.Hq, w.Hkv, w.d, w.dtype_code, h) for h in range(w.Hkv)])
+    assert np.allclose(heads.mean(axis=0), avg, rtol=1e-14, atol=0)
+    bound = 4e-6 * np.maximum(np.abs(heads), 1.0).mean(axis=0) + w.Hkv * 2.0 ** -24 * np.abs(heads).mean(axis=0)
+    g = scores.cpu().numpy().astype(np.float64)
+    worst = 0.0
     for r in range(w.B):
         b0, n = int(w.blk_off[r]), int(w.n_blocks[r])
         mid = slice(b0 + w.n_sink, b0 + max(n - w.n_local, w.n_sink))
-        assert np.allclose(g[mid], avg[mid], rtol=2e-5, atol=2e-4 * np.abs(avg).max())
+        err = np.abs(g[mid] - avg[mid])
+        assert np.all(err <= bound[mid]), (r, float((err / bound[mid]).max()))
+        if err.size:
+            worst = max(worst, float((err / bound[mid]).max()))
+    say(f"  average scores: worst error {worst:.2f} of the fp32 bound")
     say(f"  {w.B} requests, {w.total_blocks} blocks, {n_ties} near-tie differences")
 
 
