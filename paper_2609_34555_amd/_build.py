@@ -1,11 +1,14 @@
 """Build libpulse.so (the gfx950 kernels + C ABI) in-tree with hipcc.
 
-Cross-compiles for gfx950 without a GPU.  Packed-fp32 instructions are
-disabled for all device code.
+Cross-compiles for gfx950 without a GPU: every source is compiled to an object
+in parallel, then the objects are linked into one shared library.  Packed-fp32
+instructions are disabled for all device code.
 """
 import glob
 import os
 import subprocess
+import tempfile
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
@@ -17,33 +20,45 @@ FLAGS = [
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-fvisibility=hidden",
 ]
 
-
 LIBS = ["-lrocblas"]  # the normal-batch FFN GEMMs of the layer scheduler
+
+# the host pass does not know the packed-fp32 target feature; that warning is harmless
+_NOISE = "is not a recognized feature for this target"
 
 
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
 
 
-def build_library(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC] + FLAGS + ["-I", os.path.join(HERE, "..", "include")] + sources() + LIBS + ["-o", tmp]
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
-    # the host pass does not know the packed-fp32 target feature; that warning is harmless
-    noise = "is not a recognized feature for this target"
-    msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if noise not in ln and ln.strip()]
+    msgs = [ln for ln in (res.stdout + res.stderr).splitlines() if _NOISE not in ln and ln.strip()]
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + "\n".join(msgs))
     if verbose and msgs:
-        print("\n".join(msgs))
+        print("\n".join(msgs), flush=True)
+
+
+def build_library(verbose: bool = False, jobs: int = 8) -> str:
+    inc = ["-I", os.path.join(HERE, "..", "include")]
+    with tempfile.TemporaryDirectory(prefix="pulse_build_") as tmpdir:
+        objs = []
+        cmds = []
+        for src in sources():
+            obj = os.path.join(tmpdir, os.path.basename(src) + ".o")
+            objs.append(obj)
+            cmds.append([HIPCC] + FLAGS + inc + ["-c", src, "-o", obj])
+        with ThreadPoolExecutor(max(1, min(jobs, len(cmds)))) as ex:
+            list(ex.map(lambda c: _run(c, verbose), cmds))
+        tmp = LIB + ".tmp"
+        _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + objs + LIBS + ["-o", tmp], verbose)
     os.replace(tmp, LIB)
     return LIB
 
