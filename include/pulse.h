@@ -424,6 +424,28 @@ typedef struct {
  */
 PULSE_API pulse_status pulse_decode_layer(const pulse_layer_args* args, pulse_stream_t stream);
 
+/*
+ * pulse_decode_layer for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * workspace comes from a static device array of PULSE_NOALLOC_SCRATCH_BYTES
+ * that the library holds on each GPU it runs on until the process ends, so the
+ * caller passes args->ws = NULL and args->ws_bytes = 0 (else
+ * PULSE_ERR_INVALID_ARG) and still owns every input and output buffer.  A call
+ * whose workspace (pulse_workspace_bytes(shape, B, k_max, total_blocks)) would
+ * exceed that size returns PULSE_ERR_WORKSPACE and enqueues nothing.  The
+ * first call on a device looks up that device's array (no allocation); a
+ * failed lookup returns PULSE_ERR_HIP.  Results are those of
+ * pulse_decode_layer with a workspace of its own.
+ * Every call on one GPU shares that GPU's array and finds there what the last
+ * call left: calls that overlap on one GPU (concurrent streams, threads) race
+ * and must not be made.  Each call writes every workspace word it reads, except
+ * release_previous, which reads the plan the previous call left: it is valid only
+ * when the previous call on this GPU was pulse_decode_layer_noalloc with the same
+ * B, k_max and total_blocks on the same table, free list and statistics.
+ */
+#define PULSE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+PULSE_API pulse_status pulse_decode_layer_noalloc(const pulse_layer_args* args, pulse_stream_t stream);
+
 /* ---- Interruptible layer-wise scheduling (IRQ, Sec. 4.2) ---- */
 
 /*

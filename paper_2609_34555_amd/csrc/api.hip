@@ -3,6 +3,8 @@
 // kernel launches.  Nothing here allocates device memory or synchronises.
 #include <string.h>
 
+#include <mutex>
+
 #include "pulse_internal.h"
 
 namespace pulse {
@@ -423,6 +425,52 @@ pulse_status pulse_decode_layer(const pulse_layer_args* a, pulse_stream_t stream
     if (layer_recall(*a, hs, 8, E(2), E(3)) != hipSuccess) return PULSE_ERR_HIP;
     if (layer_attention(*a, hs, E(4)) != hipSuccess) return PULSE_ERR_HIP;
     return PULSE_OK;
+}
+
+}  // extern "C"
+
+namespace pulse {
+
+// Workspace of pulse_decode_layer_noalloc: one array per GPU, kept for the life of
+// the process.  In host code `scratch` names a host-side stand-in, not device
+// memory: the device address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) uint8_t scratch[PULSE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch array; nullptr on a HIP error.
+static void* scratch_for_current_device() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        g_scratch_ptr[dev] = p;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace pulse
+
+extern "C" {
+
+pulse_status pulse_decode_layer_noalloc(const pulse_layer_args* args, pulse_stream_t stream) {
+    PULSE_REQUIRE(args, PULSE_ERR_INVALID_ARG);
+    PULSE_REQUIRE(!args->ws && args->ws_bytes == 0, PULSE_ERR_INVALID_ARG);
+    pulse_layer_args a = *args;
+    // other argument errors are reported by pulse_decode_layer's own checks
+    if (shape_supported(&a.shape) && a.B > 0 && a.B <= kMaxBatch && a.k_max >= 1 && a.total_blocks >= 0) {
+        const size_t need = ws_layout(a.shape, a.B, a.k_max, a.total_blocks).total;
+        PULSE_REQUIRE(need <= (size_t)PULSE_NOALLOC_SCRATCH_BYTES, PULSE_ERR_WORKSPACE);
+        void* ws = scratch_for_current_device();
+        if (!ws) return PULSE_ERR_HIP;
+        a.ws = ws;
+        a.ws_bytes = need;
+    }
+    return pulse_decode_layer(&a, stream);
 }
 
 pulse_status pulse_probe_hbm_read(const void* src, size_t bytes, void* sink, void* start_event, void* stop_event,

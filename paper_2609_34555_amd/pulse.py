@@ -23,12 +23,15 @@ PULSE_ERR_SELECT_OVERFLOW = 5
 PULSE_ERR_HIP = 6
 PULSE_ERR_BAD_INDEX = 7
 PULSE_ERR_TIMEOUT = 8
+
+NOALLOC_SCRATCH_BYTES = 32 << 20  # PULSE_NOALLOC_SCRATCH_BYTES: static workspace of pulse_decode_layer_noalloc
 PULSE_F16 = 0
 PULSE_BF16 = 1
 
 EXPORTED = (
     "pulse_status_string", "pulse_block_bytes", "pulse_workspace_bytes", "pulse_build_digests",
     "pulse_select_solohead", "pulse_recall_gather", "pulse_sparse_decode_attn", "pulse_decode_layer",
+    "pulse_decode_layer_noalloc",
     "pulse_host_alloc", "pulse_host_free", "pulse_baseline_memcpy_units", "pulse_probe_host_read",
     "pulse_events_create", "pulse_events_destroy", "pulse_event_elapsed_ms", "pulse_headwise_workspace_bytes",
     "pulse_select_headwise", "pulse_gs_engine_create", "pulse_gs_engine_destroy", "pulse_gs_recall_submit",
@@ -130,6 +133,7 @@ def lib():
             "pulse_sparse_decode_attn": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, F, _P, _P,
                                                         _P, _P, SZ, _P]),
             "pulse_decode_layer": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
+            "pulse_decode_layer_noalloc": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
             "pulse_host_alloc": (ctypes.c_int, [SZ, I32, ctypes.POINTER(ctypes.c_void_p)]),
             "pulse_host_free": (ctypes.c_int, [_P]),
             "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
@@ -359,6 +363,11 @@ def pulse_sparse_decode_attn(shape, q, slot_pool, n_slots, block_table, max_bloc
 def pulse_decode_layer(args: pulse_layer_args, stream=None, check=True):
     st = lib().pulse_decode_layer(ctypes.byref(args), _stream(stream))
     return _check(st, "pulse_decode_layer", check)
+
+
+def pulse_decode_layer_noalloc(args: pulse_layer_args, stream=None, check=True):
+    st = lib().pulse_decode_layer_noalloc(ctypes.byref(args), _stream(stream))
+    return _check(st, "pulse_decode_layer_noalloc", check)
 
 
 def pulse_host_alloc(nbytes: int, coherent: bool = True) -> int:

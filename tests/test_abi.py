@@ -104,6 +104,38 @@ def test_decode_layer_validation_codes():
     assert P.lib().pulse_decode_layer(None, None) == P.PULSE_ERR_INVALID_ARG
 
 
+def test_decode_layer_noalloc_validation_codes():
+    """The static-workspace variant: a caller workspace is refused, a call needing more than
+    the static array is refused before any device work, B = 0 does nothing."""
+    la = P.pulse_layer_args()
+    la.shape = shape()
+    la.B = 2
+    la.total_blocks = 10
+    for f in ("ctx_len", "blk_off", "q", "digests", "k_mid", "sel_idx", "sel_cnt", "host_kv", "block_table",
+              "free_slots", "free_head", "slot_pool", "stats", "out", "dev_status"):
+        setattr(la, f, FAKE)
+    la.k_max, la.max_blocks, la.n_free, la.n_slots, la.n_sink_blocks, la.n_local_blocks = 16, 100, 10, 50, 1, 8
+    la.ws, la.ws_bytes = FAKE, 1 << 20
+    assert P.pulse_decode_layer_noalloc(la, stream=0, check=False) == P.PULSE_ERR_INVALID_ARG
+    la.ws, la.ws_bytes = None, 0
+    # the largest total_blocks whose workspace fits, and one more block than that
+    fit = (P.NOALLOC_SCRATCH_BYTES - P.pulse_workspace_bytes(la.shape, 2, 16, 0)) // 4
+    assert P.pulse_workspace_bytes(la.shape, 2, 16, fit) <= P.NOALLOC_SCRATCH_BYTES
+    la.total_blocks = fit + 256
+    assert P.pulse_workspace_bytes(la.shape, 2, 16, la.total_blocks) > P.NOALLOC_SCRATCH_BYTES
+    assert P.pulse_decode_layer_noalloc(la, stream=0, check=False) == P.PULSE_ERR_WORKSPACE
+    la.total_blocks = 10
+    la.shape = shape(head_dim=64)
+    assert P.pulse_decode_layer_noalloc(la, stream=0, check=False) == P.PULSE_ERR_UNSUPPORTED
+    la.shape = shape()
+    la.B = 0
+    assert P.pulse_decode_layer_noalloc(la, stream=0, check=False) == P.PULSE_OK
+    assert P.lib().pulse_decode_layer_noalloc(None, None) == P.PULSE_ERR_INVALID_ARG
+    text = open(HEADER).read()
+    assert re.search(r"#define PULSE_NOALLOC_SCRATCH_BYTES \(\(size_t\)32 << 20\)", text)
+    assert P.NOALLOC_SCRATCH_BYTES == 32 << 20
+
+
 def test_probe_and_baseline_validation():
     assert P.pulse_probe_host_read(FAKE, FAKE, 1000, stream=0, check=False) == P.PULSE_ERR_INVALID_ARG
     assert P.pulse_baseline_memcpy_units(FAKE, FAKE, FAKE, FAKE, 0, 4096, stream=0, check=False) == P.PULSE_OK

@@ -1,0 +1,79 @@
+"""pulse_decode_layer_noalloc -- a layer-step whose workspace is the library's static
+per-GPU array -- against pulse_decode_layer with a caller workspace, through the C ABI.
+Two calls in a row, the second on a smaller workload (the array keeps the first call's
+contents), then two release_previous steps; every output must be bit-identical to the
+workspace path's and match the CPU oracle."""
+import pytest
+import torch
+
+from paper_2609_34555_amd import harness as H
+from paper_2609_34555_amd import pulse as P
+from paper_2609_34555_amd import workloads as W
+
+from parity import build, full_check, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _state(st):
+    torch.cuda.synchronize()
+    return dict(status=st.status(), sel_idx=st.sel_idx.clone(), sel_cnt=st.sel_cnt.clone(), table=st.table.clone(),
+                free_head=st.free_head.clone(), stats=st.stats.clone(), pool=st.pool.clone(), out=st.out.clone(),
+                lse=st.lse.clone())
+
+
+def _assert_same(a, b):
+    for k in a:
+        if k == "status":
+            assert a[k] == b[k] == 0, (a[k], b[k])
+        else:
+            assert torch.equal(a[k], b[k]), k
+
+
+def _noalloc_args(st, release_previous=False):
+    a = st.layer_args(release_previous=release_previous)
+    a.ws = None
+    a.ws_bytes = 0
+    return a
+
+
+@pytest.fixture(scope="module")
+def workloads():
+    big = W.preset(2, ctx_scale=1 / 4)  # 8 x 8K tokens, bf16, G 4
+    small = W.preset(1)                 # 1 x 4K tokens, fp16: a smaller workspace
+    return [big, small]
+
+
+def test_noalloc_matches_workspace_path_on_two_calls(workloads):
+    for i, (spec, seed) in enumerate(workloads):
+        say(f"\n[gpu] noalloc call {i}: {spec.name if hasattr(spec, 'name') else spec}")
+        w, ref = build(spec, seed)
+        st = H.LayerState(w, ref.host_ptr)
+        ref.reset()
+        P.pulse_decode_layer(ref.layer_args())
+        want = _state(ref)
+        st.reset()
+        P.pulse_decode_layer_noalloc(_noalloc_args(st))
+        got = _state(st)
+        _assert_same(got, want)
+        res = full_check(w, st, run=False)
+        say(f"  ws {ref.ws_bytes} B; stats={res['stats']} attn_err={res['attn_err'][0]:.1e}")
+        del st, ref
+        torch.cuda.empty_cache()
+
+
+def test_noalloc_release_previous_steps(workloads):
+    """Two layer-steps with release_previous (the second undoes the first's recall inside its
+    scoring kernel, reading the plan the first left in the static array)."""
+    spec, seed = workloads[0]
+    w, ref = build(spec, seed)
+    st = H.LayerState(w, ref.host_ptr)
+    for s, call in ((ref, lambda a: P.pulse_decode_layer(a)), (st, lambda a: P.pulse_decode_layer_noalloc(a))):
+        s.reset()
+        for k in range(2):
+            a = s.layer_args(release_previous=k > 0)
+            if s is st:
+                a.ws, a.ws_bytes = None, 0
+            call(a)
+    _assert_same(_state(st), _state(ref))
+    full_check(w, st, run=False)
