@@ -5,14 +5,18 @@ A step = digest score + SoloHead selection (with the set difference) + slot
 allocation and gather-scatter recall from pinned host DRAM + sparse GQA
 decode attention, chained on one stream by pulse_decode_layer.
 
-Workload (synthetic, seeded): 8 requests x 32K tokens, block 16, 32 query /
-8 KV heads, head_dim 128, bf16, 2048-token hot budget (1 sink + 8 local + 119
-middle blocks), 10% of blocks resident, 32 planted heavy blocks per request.
-The queries, digests, block table and slot pool are in HBM and the full KV
-store is in pinned host DRAM when the timed region starts (the host tier is
-the method's own data structure).
+Default workload (synthetic, seeded; the largest single-layer configuration):
+32 requests with contexts drawn uniformly from [64K, 128K] tokens (ragged block
+tables, partial last blocks), block 16, 32 query / 8 KV heads, head_dim 128,
+bf16, 4096-token hot budget (1 sink + 8 local + 247 middle blocks), 5% of
+blocks resident, 32 planted heavy blocks per request.  The queries, digests,
+block table and slot pool are in HBM and the full KV store (12 GiB) is in
+pinned host DRAM when the timed region starts (the host tier is the method's
+own data structure).
 
 Prints one JSON line.  value = recall bytes per step / wall time per step.
+With the default preset the line also carries a `presets` sub-record: the
+other four workloads, each timed the same way (without CPU baseline or probes).
 """
 import argparse
 import json
@@ -32,8 +36,10 @@ HBM_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5],
-                    help="workload preset (2 = the default benchmark line)")
+    ap.add_argument("--config", type=int, default=3, choices=[1, 2, 3, 4, 5],
+                    help="workload preset (3 = the default benchmark line)")
+    ap.add_argument("--no-presets", action="store_true",
+                    help="with the default preset: leave out the sub-record of the other four presets")
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -48,9 +54,13 @@ def parse():
                     help="report: recall bandwidth against the number of blocks per recall for the GPU gather "
                          "kernel, the paper's engine and one hipMemcpyAsync per block (not the default line)")
     ap.add_argument("--normal-batch", type=int, default=32)
+    ap.add_argument("--summarize-counters", nargs="+", metavar="DIR",
+                    help="no GPU work: turn rocprofv3 --pmc output directories of `bench.py --profile --config N` "
+                         "(FETCH_SIZE, WRITE_SIZE, optionally TCC_EA0_RDREQ_sum / _32B_sum / TCC_BUBBLE_sum) into "
+                         "profiles/counters_cfgN.json and print a markdown table")
     ap.add_argument("--profile", action="store_true",
-                    help="profiler run: no CPU baseline or link probes; adds one 256 MiB device copy "
-                         "that calibrates the byte counters")
+                    help="profiler run: no CPU baseline, link probes or preset sub-record; adds device copies "
+                         "of known size that calibrate the byte counters")
     return ap.parse_args()
 
 
@@ -135,12 +145,13 @@ def memcpy_recall_baseline(torch, P, st, w):
     return {"blocks": len(src), "ms": ms, "GBps": len(src) * w.unit_bytes / (ms * 1e-3) / 1e9}
 
 
-def counter_traffic(kernel):
-    """HBM-side bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE/WRITE_SIZE
-    passes (scaled by the copy-kernel calibration); None if its sources changed since."""
+def counter_traffic(kernel, cid):
+    """HBM-side bytes per launch of `kernel` on preset `cid` from the committed rocprofv3
+    FETCH_SIZE/WRITE_SIZE passes (scaled by the copy-kernel calibration); None if there are
+    none for this preset or the kernel's sources changed since."""
     import hashlib
 
-    path = os.path.join(ROOT, "profiles", "counters_cfg2.json")
+    path = os.path.join(ROOT, "profiles", f"counters_cfg{cid}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -153,7 +164,93 @@ def counter_traffic(kernel):
             h.update(f.read())
     if h.hexdigest()[:16] != k["sources_sha256_16"]:
         return None
+    if "fetch_bytes" not in k:
+        return None
     return {"fetch": k["fetch_bytes"], "write": k["write_bytes"], "total": k["fetch_bytes"] + k["write_bytes"]}
+
+
+KERNEL_SOURCES = {
+    "recall_copy_kernel": ["paper_2609_34555_amd/csrc/recall.hip", "paper_2609_34555_amd/csrc/pulse_internal.h"],
+    "attn_splitk_kernel": ["paper_2609_34555_amd/csrc/attention.hip", "paper_2609_34555_amd/csrc/pulse_internal.h"],
+    "attn_combine_kernel": ["paper_2609_34555_amd/csrc/attention.hip", "paper_2609_34555_amd/csrc/pulse_internal.h"],
+    "score_kernel": ["paper_2609_34555_amd/csrc/digest.hip", "paper_2609_34555_amd/csrc/pulse_internal.h"],
+    "select_kernel": ["paper_2609_34555_amd/csrc/select.hip", "paper_2609_34555_amd/csrc/pulse_internal.h"],
+}
+
+
+def _sources_hash(files):
+    import hashlib
+
+    h = hashlib.sha256()
+    for src in files:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def summarize_counters(dirs, cid):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of a profiler run of this file, scaled to bytes
+    by the reading of the calibration copies (probe_copy_kernel over CALIBRATION_COPIES bytes,
+    device to device, one dispatch per size in order).  With a third directory holding
+    TCC_EA0_RDREQ_sum / TCC_EA0_RDREQ_32B_sum / TCC_BUBBLE_sum, the read requests are reported
+    too (the calibration shows their size).  Writes profiles/counters_cfg{cid}.json."""
+    import collections
+    import csv
+
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for d in dirs:
+        with open(os.path.join(d, "bench_counter_collection.csv")) as f:
+            for r in csv.DictReader(f):
+                name = r["Kernel_Name"].split("(")[0].replace("void ", "").strip()
+                vals[name][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    cal = vals["pulse::probe_copy_kernel"]
+    if len(cal["FETCH_SIZE"]) != len(CALIBRATION_COPIES) or len(cal["WRITE_SIZE"]) != len(CALIBRATION_COPIES):
+        raise RuntimeError("expected one calibration copy dispatch per size")
+    fetch_f = [b / (k * 1024) for b, k in zip(CALIBRATION_COPIES, cal["FETCH_SIZE"])]
+    write_f = [b / (k * 1024) for b, k in zip(CALIBRATION_COPIES, cal["WRITE_SIZE"])]
+    fs, ws = statistics.mean(fetch_f), statistics.mean(write_f)
+    calib = {"copy_bytes": list(CALIBRATION_COPIES), "fetch_KiB": cal["FETCH_SIZE"], "write_KiB": cal["WRITE_SIZE"],
+             "fetch_scale_per_size": fetch_f, "write_scale_per_size": write_f, "fetch_scale": fs, "write_scale": ws}
+    if "TCC_EA0_RDREQ_sum" in cal:
+        calib["rdreq"] = cal["TCC_EA0_RDREQ_sum"]
+        calib["rdreq_32B"] = cal.get("TCC_EA0_RDREQ_32B_sum")
+        calib["bubble"] = cal.get("TCC_BUBBLE_sum")
+        calib["bytes_per_read_request"] = [b / n for b, n in zip(CALIBRATION_COPIES, cal["TCC_EA0_RDREQ_sum"])]
+    out = {"preset": cid, "workload": WORKLOADS[cid], "calibration": calib, "kernels": {}}
+    rows = []
+    for name in sorted(vals):
+        if not name.startswith("pulse::") or "probe" in name:
+            continue
+        v = vals[name]
+        fa, wa = statistics.mean(v["FETCH_SIZE"]), statistics.mean(v.get("WRITE_SIZE", [0.0]))
+        rec = {"dispatches": len(v["FETCH_SIZE"]), "fetch_KiB": fa, "write_KiB": wa,
+               "fetch_bytes": fa * 1024 * fs, "write_bytes": wa * 1024 * ws}
+        if "TCC_EA0_RDREQ_sum" in v:
+            rec["read_requests"] = statistics.mean(v["TCC_EA0_RDREQ_sum"])
+            rec["read_requests_32B"] = statistics.mean(v["TCC_EA0_RDREQ_32B_sum"])
+            rec["bubble"] = statistics.mean(v["TCC_BUBBLE_sum"])
+        short = name.split("::")[1].split("<")[0]
+        if short in KERNEL_SOURCES:
+            rec["sources"] = KERNEL_SOURCES[short]
+            rec["sources_sha256_16"] = _sources_hash(KERNEL_SOURCES[short])
+            out["kernels"][short] = rec
+        rows.append((name, rec))
+    path = os.path.join(ROOT, "profiles", f"counters_cfg{cid}.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(f"calibration: FETCH scale {fs:.4f} ({', '.join(f'{x:.4f}' for x in fetch_f)}), "
+          f"WRITE scale {ws:.4f} ({', '.join(f'{x:.4f}' for x in write_f)})")
+    if "bytes_per_read_request" in calib:
+        print("bytes per read request of the calibration copies: "
+              + ", ".join(f"{x:.2f}" for x in calib["bytes_per_read_request"]) + f"; TCC_BUBBLE {calib['bubble']}")
+    print("| Kernel | Dispatches | FETCH_SIZE (KiB, avg) | WRITE_SIZE (KiB, avg) | Fetch bytes (scaled) | "
+          "Write bytes (scaled) | Read requests (avg) |")
+    print("|---|---|---|---|---|---|---|")
+    for name, r in rows:
+        rq = f"{r['read_requests']:,.0f}" if "read_requests" in r else "-"
+        print(f"| `{name}` | {r['dispatches']} | {r['fetch_KiB']:.1f} | {r['write_KiB']:.1f} | {r['fetch_bytes']:,.0f} | "
+              f"{r['write_bytes']:,.0f} | {rq} |")
+    return out
 
 
 def engine_recall_baseline(torch, P, st, w, reps=5):
@@ -463,7 +560,50 @@ def rooflines(w, st, timed, mean, rbytes, peak_measured):
     return roof, attn_roof, score_roof
 
 
-def bench_layer(cid, args, torch, P, H, W):
+CALIBRATION_COPIES = (64 << 20, 256 << 20, 1 << 30)  # device-to-device copies that scale the byte counters
+
+
+def calibration_copies(torch, P):
+    """Profiler runs only: device-to-device copies of known size through the library's streaming
+    copy kernel (probe_copy_kernel: the recall's 16-byte load / store pattern), one dispatch per
+    size in CALIBRATION_COPIES order, then one runtime copy (the hipMemcpy blit kernel) of 256 MiB.
+    FETCH_SIZE / WRITE_SIZE of these dispatches give the factors that turn the counters into bytes."""
+    n = max(CALIBRATION_COPIES)
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(3)
+    torch.cuda.synchronize()
+    for nbytes in CALIBRATION_COPIES:
+        P.pulse_probe_host_read(a, b, nbytes)
+        torch.cuda.synchronize()
+    b[: 256 << 20].copy_(a[: 256 << 20])
+    torch.cuda.synchronize()
+    if not torch.equal(a[: 256 << 20], b[: 256 << 20]):
+        raise RuntimeError("calibration copy mismatch")
+    del a, b
+    return {"probe_copy_kernel_bytes": list(CALIBRATION_COPIES), "runtime_copy_bytes": 256 << 20}
+
+
+def attach_traffic(cid, roof, attn_roof, score_roof):
+    """`traffic` of each roofline from the committed counter passes of this preset (null when
+    there are none, or the kernel's sources changed since they were taken)."""
+    rec = counter_traffic("recall_copy_kernel", cid)
+    roof["traffic"] = (rec or {}).get("total")
+    roof["traffic_split"] = rec
+    if rec is not None:
+        roof["traffic_note"] = ("fetch = the blocks read from pinned host memory over the link, write = the "
+                                "same bytes stored to the HBM slot pool: each is bytes_per_launch, no re-reads")
+    attn = counter_traffic("attn_splitk_kernel", cid)
+    attn_roof["traffic"] = (attn or {}).get("total")
+    attn_roof["traffic_split"] = attn
+    score = counter_traffic("score_kernel", cid)
+    score_roof["traffic"] = (score or {}).get("total")
+    score_roof["traffic_split"] = score
+
+
+def bench_layer(cid, args, torch, P, H, W, compact=False):
+    """One workload preset: K timed layer-steps plus untimed event passes.  compact: no
+    profiler calibration, link / HBM probes or CPU baseline (the presets sub-record)."""
     spec, seed = W.preset(cid)
     holder = []
     t0 = time.time()
@@ -480,41 +620,23 @@ def bench_layer(cid, args, torch, P, H, W):
     ms_per_step = wall * 1e3 / K
 
     extras = {}
-    if args.profile:
-        # calibration kernel for the FETCH_SIZE / WRITE_SIZE counters: 256 MiB read + 256 MiB written
-        a = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
-        b = torch.empty_like(a)
-        a.fill_(3)
-        torch.cuda.synchronize()
-        b.copy_(a)
-        torch.cuda.synchronize()
-        extras["calibration_copy_bytes"] = 256 << 20
-        del a, b
-        args.no_cpu_baseline = True
-        args.no_probes = True
-    if not args.no_probes:
+    probes = not (args.no_probes or args.profile or compact)
+    if args.profile and not compact:
+        extras["calibration"] = calibration_copies(torch, P)
+    if probes:
         extras["link"] = link_probes(torch, P, st, holder)
         extras["per_block_memcpy_recall"] = memcpy_recall_baseline(torch, P, st, w)
         extras["paper_engine_recall"] = engine_recall_baseline(torch, P, st, w)
     peak_measured = max([extras["link"]["memcpy_1GiB_GBps"], extras["link"]["kernel_read_1GiB_GBps"]]
                         if "link" in extras else [0.0]) or None
     roof, attn_roof, score_roof = rooflines(w, st, timed, mean, rbytes, peak_measured)
-    if not args.no_probes:  # measured HBM read ceilings at the kernels' own sizes, and at 1 GiB
+    if probes:  # measured HBM read ceilings at the kernels' own sizes, and at 1 GiB
         for r in (attn_roof, score_roof):
             r["peak_measured"] = hbm_probe(torch, P, r["bytes_per_launch"])
             r["frac_of_measured"] = r["achieved"] / r["peak_measured"]
         extras["hbm_read_1GiB_GBps"] = hbm_probe(torch, P, 1 << 30)
         attn_roof["isolated"] = attention_warm_cold(torch, st, attn_roof["bytes_per_launch"])
-    if cid == 2:  # the committed counter passes were taken on this workload
-        roof["traffic"] = (counter_traffic("recall_copy_kernel") or {}).get("total")
-        roof["traffic_split"] = counter_traffic("recall_copy_kernel")
-        if roof["traffic"] is not None:
-            roof["traffic_note"] = ("fetch = the blocks read from pinned host memory over the link, write = the "
-                                    "same bytes stored to the HBM slot pool: each is bytes_per_launch, no re-reads")
-        attn_roof["traffic"] = (counter_traffic("attn_splitk_kernel") or {}).get("total")
-        score_roof["traffic"] = (counter_traffic("score_kernel") or {}).get("total")
-    else:
-        roof["traffic"] = None
+    attach_traffic(cid, roof, attn_roof, score_roof)
     line = base_line(cid, K, args.warmup)
     line.update({
         "value": rbytes / (ms_per_step * 1e-3) / 1e9,
@@ -533,12 +655,44 @@ def bench_layer(cid, args, torch, P, H, W):
         "extras": extras,
         "setup_s": {"generate": gen_s},
     })
-    if not args.no_cpu_baseline:
+    if not (args.no_cpu_baseline or args.profile or compact):
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    del st, w
+    for store in holder:
+        store.free()
+    torch.cuda.empty_cache()
     return line
 
 
-def bench_multilayer(args, torch, P, H, W):
+def presets_record(args, torch, P, H, W):
+    """The other four presets, each timed as the default line (K steps after W warm-ups) but
+    without probes or CPU baseline: a compact record per preset."""
+    keep = ("value", "unit", "us_per_layer_step", "ms_per_step", "dtype", "config", "recall", "stage_us",
+            "schedules_ms", "headwise_vs_solohead", "attention_ms_per_step")
+    out = {}
+    for cid in (1, 2, 4, 5):
+        t = time.time()
+        if cid == 4:
+            line = bench_multilayer(args, torch, P, H, W, compact=True)
+        else:
+            line = bench_layer(cid, args, torch, P, H, W, compact=True)
+        rec = {k: line[k] for k in keep if k in line}
+        rec["roofline"] = {k: line["roofline"].get(k) for k in ("bound", "achieved", "peak", "frac", "traffic")}
+        for name in ("roofline_hbm_attention", "roofline_hbm_score"):
+            if name in line:
+                r = line[name]
+                rec[name] = {"achieved": r["achieved"], "peak": r["peak"], "frac": r["frac"],
+                             "traffic": r.get("traffic")}
+                if "with_combine" in r:
+                    rec[name]["with_combine_frac"] = r["with_combine"]["frac"]
+        rec["wall_s"] = time.time() - t
+        out[str(cid)] = rec
+        print(f"[bench] preset {cid}: {rec['value']:.2f} GB/s, {rec['us_per_layer_step']:.1f} us per layer-step",
+              file=sys.stderr, flush=True)
+    return out
+
+
+def bench_multilayer(args, torch, P, H, W, compact=False):
     """Preset 4: a 32-layer decode step.  Timed: the two-stream schedule (recall of
     layer l+1 overlapping attention of layer l); also reported: the same step chained on
     one stream, and headwise vs SoloHead recall transfers."""
@@ -619,8 +773,10 @@ def bench_multilayer(args, torch, P, H, W):
         "attention_ms_per_step": attn_ms,
         "setup_s": {"generate_and_upload": gen_s},
     })
-    if not args.no_cpu_baseline:
+    if not (args.no_cpu_baseline or args.profile or compact):
         line["cpu_baseline"] = cpu_baseline(w0, args.cpu_seconds, "layer 0 of the 32-layer step")
+    del ml
+    torch.cuda.empty_cache()
     return line
 
 
@@ -802,6 +958,9 @@ def bench_recall_sweep(args, torch, P, H, W):
 
 def main():
     args = parse()
+    if args.summarize_counters:
+        summarize_counters(args.summarize_counters, args.config)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the sparse-KV decode path here has no multi-GPU mode "
@@ -825,6 +984,8 @@ def main():
         line = bench_multilayer(args, torch, P, H, W)
     else:
         line = bench_layer(args.config, args, torch, P, H, W)
+    if args.config == 3 and not (args.no_presets or args.profile):
+        line["presets"] = presets_record(args, torch, P, H, W)
     print(json.dumps(line), flush=True)
 
 

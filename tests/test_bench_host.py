@@ -61,10 +61,21 @@ def test_counter_traffic_only_for_unchanged_sources(tmp_path, monkeypatch):
         "same": {"fetch_bytes": 3.0, "write_bytes": 4.0, "sources": ["k.hip"], "sources_sha256_16": good},
         "changed": {"fetch_bytes": 3.0, "write_bytes": 4.0, "sources": ["k.hip"], "sources_sha256_16": "0" * 16}}}
     (tmp_path / "profiles").mkdir()
-    (tmp_path / "profiles" / "counters_cfg2.json").write_text(json.dumps(data))
+    (tmp_path / "profiles" / "counters_cfg3.json").write_text(json.dumps(data))
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.counter_traffic("same") == {"fetch": 3.0, "write": 4.0, "total": 7.0}
-    assert bench.counter_traffic("changed") is None
-    assert bench.counter_traffic("absent") is None
+    assert bench.counter_traffic("same", 3) == {"fetch": 3.0, "write": 4.0, "total": 7.0}
+    assert bench.counter_traffic("same", 2) is None  # no passes taken on that preset
+    assert bench.counter_traffic("changed", 3) is None
+    assert bench.counter_traffic("absent", 3) is None
     src.write_text("edited\n")
-    assert bench.counter_traffic("same") is None
+    assert bench.counter_traffic("same", 3) is None
+
+
+def test_default_line_is_the_largest_single_layer_preset(monkeypatch):
+    """With no flags the benchmark runs preset 3 (32 requests x U[64K,128K] tokens)."""
+    import sys
+
+    monkeypatch.setattr(sys, "argv", [bench.__file__])
+    args = bench.parse()
+    assert args.config == 3 and args.gpus == 1 and not args.no_presets
+    assert "U[65536,131072]" in bench.WORKLOADS[3]
