@@ -8,8 +8,9 @@ Definitions followed:
   - the overlap depth is profiled offline on a grid of (B_o, B_n) and interpolated
     from the nearest profiled points (Sec. 4.3.2);
   - each waiting request is admitted to the normal batch or offloaded; branches over
-    the GPU memory budget are infeasible; once a longer request is admitted to the
-    normal batch, shorter requests are not offloaded (Sec. 4.3.1).
+    the GPU memory budget are infeasible; length monotonicity: after the longest
+    normal-batch admission on a path, no shorter request goes to the offload batch
+    (Sec. 4.3.1).
 Readings taken where the paper is silent:
   I1  requests are decided longest first; when a request fits neither batch, it and
       every later request keep waiting (the search stops on that path);

@@ -30,9 +30,12 @@ _lib = None
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
-            _build.build_oracle()
-        lib = ctypes.CDLL(_build.LIB)
+        path = os.environ.get("PULSE_ORACLE_LIB")  # another build of pulse_oracle.c (sanitizer runs)
+        if not path:
+            if not os.path.exists(_build.LIB):
+                _build.build_oracle()
+            path = _build.LIB
+        lib = ctypes.CDLL(path)
         P = ctypes.c_void_p
         I = ctypes.c_int
         lib.or_decode.restype = ctypes.c_double

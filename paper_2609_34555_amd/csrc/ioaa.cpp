@@ -8,8 +8,8 @@
 //
 // Search (Sec. 4.3.1): a depth-first walk of the binary tree whose level t
 // decides the t-th longest request (normal branch first, then offload).  Two
-// prunes: a branch that exceeds the GPU memory budget is cut, and once a longer
-// request went to the normal batch shorter ones are not offloaded.  A request
+// prunes: a branch that exceeds the GPU memory budget is cut, and length
+// monotonicity (no offload admission below a normal-batch one).  A request
 // that fits neither batch ends the path (it and all shorter ones keep
 // waiting); Eq. 1 is evaluated where a path ends.
 #include <algorithm>

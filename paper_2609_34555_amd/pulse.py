@@ -119,64 +119,75 @@ def lib():
         import torch  # noqa: F401
 
         L = ctypes.CDLL(LIB_PATH)
-        I32, I64, SZ, F = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
-        SP = ctypes.POINTER(pulse_shape)
-        sig = {
-            "pulse_status_string": (ctypes.c_char_p, [ctypes.c_int]),
-            "pulse_block_bytes": (SZ, [SP]),
-            "pulse_workspace_bytes": (SZ, [SP, I32, I32, I64]),
-            "pulse_build_digests": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, _P, _P]),
-            "pulse_select_solohead": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, I32, I32, I32, _P, _P, _P,
-                                                     _P, _P, SZ, _P]),
-            "pulse_recall_gather": (ctypes.c_int, [SP, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
-                                                   _P, _P, SZ, _P]),
-            "pulse_sparse_decode_attn": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, F, _P, _P,
-                                                        _P, _P, SZ, _P]),
-            "pulse_decode_layer": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
-            "pulse_decode_layer_noalloc": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
-            "pulse_host_alloc": (ctypes.c_int, [SZ, I32, ctypes.POINTER(ctypes.c_void_p)]),
-            "pulse_host_free": (ctypes.c_int, [_P]),
-            "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
-            "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
-            "pulse_probe_hbm_read": (ctypes.c_int, [_P, SZ, _P, _P, _P, _P]),
-            "pulse_release_recalled": (ctypes.c_int, [SP, I32, I32, I64, _P, I32, _P, _P, _P, _P, SZ, _P]),
-            "pulse_probe_hbm_sink_bytes": (SZ, []),
-            "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
-            "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
-                                                     _P, _P, _P, _P, _P, SZ, _P]),
-            "pulse_average_workspace_bytes": (SZ, [SP, I32, I32, I64]),
-            "pulse_select_average": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, _P, _P, _P, _P,
-                                                    SZ, _P]),
-            "pulse_mam_workspace_bytes": (SZ, [SP, I32, I32]),
-            "pulse_mam": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, I32, I32, I32, F, _P, _P, _P, SZ, _P]),
-            "pulse_pick_solo_heads": (ctypes.c_int, [_P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
-            "pulse_irq_create": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_void_p)]),
-            "pulse_irq_destroy": (ctypes.c_int, [_P]),
-            "pulse_irq_step": (ctypes.c_int, [_P, ctypes.POINTER(pulse_layer_args), I32,
-                                              ctypes.POINTER(pulse_normal_layer), I32, I32, I32, _P, _P,
-                                              ctypes.POINTER(pulse_irq_stats)]),
-            "pulse_gs_engine_create": (ctypes.c_int, [SP, I32, I64, I64, ctypes.POINTER(ctypes.c_void_p)]),
-            "pulse_gs_engine_destroy": (ctypes.c_int, [_P]),
-            "pulse_gs_recall_submit": (ctypes.c_int, [_P, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
-                                                      _P, _P, SZ, ctypes.POINTER(ctypes.c_int64), _P]),
-            "pulse_gs_recall_poll": (ctypes.c_int, [_P, I64, ctypes.POINTER(ctypes.c_int32)]),
-            "pulse_gs_recall_wait": (ctypes.c_int, [_P, I64, I32]),
-            "pulse_gs_last_timing": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_float)]),
-            "pulse_overlap_depth": (ctypes.c_double, [ctypes.POINTER(pulse_ioaa_params), ctypes.c_double,
-                                                      ctypes.c_double]),
-            "pulse_ioaa_plan": (ctypes.c_int, [ctypes.POINTER(pulse_ioaa_params), _P, I32, _P,
-                                               ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
-                                               ctypes.POINTER(ctypes.c_int64)]),
-            "pulse_events_create": (ctypes.c_int, [I32, _P]),
-            "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
-            "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
-        }
-        for name, (res, args) in sig.items():
-            fn = getattr(L, name)
-            fn.restype = res
-            fn.argtypes = args
+        bind(L, signatures())
         _lib = L
     return _lib
+
+
+def bind(L, sig):
+    """Set restype / argtypes of every entry of `sig` (name -> (restype, argtypes)) on library L."""
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    return L
+
+
+def signatures():
+    """C signatures of the exported entry points, as ctypes types."""
+    I32, I64, SZ, F = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+    SP = ctypes.POINTER(pulse_shape)
+    sig = {
+        "pulse_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "pulse_block_bytes": (SZ, [SP]),
+        "pulse_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+        "pulse_build_digests": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, _P, _P]),
+        "pulse_select_solohead": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, I32, I32, I32, _P, _P, _P,
+                                                 _P, _P, SZ, _P]),
+        "pulse_recall_gather": (ctypes.c_int, [SP, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
+                                               _P, _P, SZ, _P]),
+        "pulse_sparse_decode_attn": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, F, _P, _P,
+                                                    _P, _P, SZ, _P]),
+        "pulse_decode_layer": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
+        "pulse_decode_layer_noalloc": (ctypes.c_int, [ctypes.POINTER(pulse_layer_args), _P]),
+        "pulse_host_alloc": (ctypes.c_int, [SZ, I32, ctypes.POINTER(ctypes.c_void_p)]),
+        "pulse_host_free": (ctypes.c_int, [_P]),
+        "pulse_baseline_memcpy_units": (ctypes.c_int, [_P, _P, _P, _P, I32, SZ, _P]),
+        "pulse_probe_host_read": (ctypes.c_int, [_P, _P, SZ, _P]),
+        "pulse_probe_hbm_read": (ctypes.c_int, [_P, SZ, _P, _P, _P, _P]),
+        "pulse_release_recalled": (ctypes.c_int, [SP, I32, I32, I64, _P, I32, _P, _P, _P, _P, SZ, _P]),
+        "pulse_probe_hbm_sink_bytes": (SZ, []),
+        "pulse_headwise_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+        "pulse_select_headwise": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, I32, I32, _P,
+                                                 _P, _P, _P, _P, _P, SZ, _P]),
+        "pulse_average_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+        "pulse_select_average": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, _P, I32, I32, I32, _P, _P, _P, _P, _P,
+                                                SZ, _P]),
+        "pulse_mam_workspace_bytes": (SZ, [SP, I32, I32]),
+        "pulse_mam": (ctypes.c_int, [SP, _P, _P, I32, _P, I32, _P, I32, I32, I32, F, _P, _P, _P, SZ, _P]),
+        "pulse_pick_solo_heads": (ctypes.c_int, [_P, I32, I32, ctypes.POINTER(I32), ctypes.POINTER(I32)]),
+        "pulse_irq_create": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_void_p)]),
+        "pulse_irq_destroy": (ctypes.c_int, [_P]),
+        "pulse_irq_step": (ctypes.c_int, [_P, ctypes.POINTER(pulse_layer_args), I32,
+                                          ctypes.POINTER(pulse_normal_layer), I32, I32, I32, _P, _P,
+                                          ctypes.POINTER(pulse_irq_stats)]),
+        "pulse_gs_engine_create": (ctypes.c_int, [SP, I32, I64, I64, ctypes.POINTER(ctypes.c_void_p)]),
+        "pulse_gs_engine_destroy": (ctypes.c_int, [_P]),
+        "pulse_gs_recall_submit": (ctypes.c_int, [_P, _P, _P, I32, _P, _P, I32, _P, I32, _P, _P, I32, _P, I32, _P,
+                                                  _P, _P, SZ, ctypes.POINTER(ctypes.c_int64), _P]),
+        "pulse_gs_recall_poll": (ctypes.c_int, [_P, I64, ctypes.POINTER(ctypes.c_int32)]),
+        "pulse_gs_recall_wait": (ctypes.c_int, [_P, I64, I32]),
+        "pulse_gs_last_timing": (ctypes.c_int, [_P, ctypes.POINTER(ctypes.c_float)]),
+        "pulse_overlap_depth": (ctypes.c_double, [ctypes.POINTER(pulse_ioaa_params), ctypes.c_double,
+                                                  ctypes.c_double]),
+        "pulse_ioaa_plan": (ctypes.c_int, [ctypes.POINTER(pulse_ioaa_params), _P, I32, _P,
+                                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_int64),
+                                           ctypes.POINTER(ctypes.c_int64)]),
+        "pulse_events_create": (ctypes.c_int, [I32, _P]),
+        "pulse_events_destroy": (ctypes.c_int, [I32, _P]),
+        "pulse_event_elapsed_ms": (ctypes.c_int, [_P, _P, ctypes.POINTER(ctypes.c_float)]),
+    }
+    return sig
 
 
 def _ptr(x):

@@ -1,11 +1,29 @@
 """IO-Adaptive Offloading Admission (Sec. 4.3): oracle pins and library parity (CPU)."""
+import ctypes
 import math
+import os
 
 import numpy as np
 import pytest
 
 from oracle import ioaa as OI
 from paper_2609_34555_amd import pulse as P
+
+_STATUS = {P.PULSE_OK: "PULSE_OK", P.PULSE_ERR_INVALID_ARG: "PULSE_ERR_INVALID_ARG"}
+
+
+@pytest.fixture(autouse=True)
+def _sanitized_build(monkeypatch):
+    """PULSE_SANITIZED_IOAA_LIB names a sanitizer build of the host-only admission search
+    (csrc/ioaa.cpp alone, built by tests/test_sanitizers.py): bind the calls of this file to it
+    instead of libpulse.so, whose GPU runtime is not loaded under the sanitizers."""
+    path = os.environ.get("PULSE_SANITIZED_IOAA_LIB")
+    if path:
+        sig = P.signatures()
+        L = P.bind(ctypes.CDLL(path), {k: sig[k] for k in ("pulse_ioaa_plan", "pulse_overlap_depth")})
+        L.pulse_status_string = lambda s: _STATUS.get(int(s), "PULSE_ERR_UNKNOWN").encode()
+        monkeypatch.setattr(P, "lib", lambda: L)
+    yield
 
 
 # ------------------------------------------------------------------ oracle pins
