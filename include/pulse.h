@@ -461,6 +461,9 @@ PULSE_API pulse_status pulse_decode_layer_noalloc(const pulse_layer_args* args, 
  *   w_gate_up bf16 [2 d_ff][D] (gate rows, then up rows); w_down bf16 [D][d_ff];
  *   x, gu, h, y bf16 scratch / output of the sizes above; out, lse as for
  *   pulse_sparse_decode_attn; ws pulse_workspace_bytes(shape, B, k_max, 0).
+ * The GEMMs (the library's MFMA kernel) read 16-byte pieces of rows: d_ff must
+ * be a multiple of 8 (else PULSE_ERR_UNSUPPORTED) and w_gate_up, w_down, x and
+ * h 16-byte aligned (else PULSE_ERR_INVALID_ARG).
  */
 typedef struct pulse_normal_layer {
     pulse_shape shape;
@@ -512,9 +515,9 @@ typedef struct pulse_irq pulse_irq;
 
 /*
  * Scheduler state for two caller-owned streams (compute, I/O; default
- * priority): a pinned host-mapped completion flag, timing events and a
- * rocBLAS handle bound to the compute stream.  Allocates; not for use inside
- * stream capture.  Destroy synchronises both streams.
+ * priority): a pinned host-mapped completion flag and timing events.
+ * Allocates; not for use inside stream capture.  Destroy synchronises both
+ * streams.
  */
 PULSE_API pulse_status pulse_irq_create(pulse_stream_t compute_stream, pulse_stream_t io_stream, pulse_irq** irq);
 PULSE_API pulse_status pulse_irq_destroy(pulse_irq* irq);

@@ -25,7 +25,7 @@ FLAGS = [
     "-fvisibility=hidden",
 ]
 
-LIBS = ["-lrocblas"]  # the normal-batch FFN GEMMs of the layer scheduler
+LIBS = []  # HIP runtime only: every kernel, the FFN GEMMs of the layer scheduler included, is built here
 
 # the host pass does not know the packed-fp32 target feature; that warning is harmless
 _NOISE = "is not a recognized feature for this target"

@@ -34,10 +34,8 @@
 // A normal-batch layer is decode attention over its resident KV (every
 // block selected; the attention kernel of this library) followed by a SwiGLU
 // FFN on the attention output: x = bf16(out), [g|u] = x W_gu^T, h = silu(g) *
-// u, y = h W_down^T (bf16, fp32 accumulation; the two GEMMs are rocBLAS
-// calls).  Projections and norms are left out.
-#include <rocblas/rocblas.h>
-
+// u, y = h W_down^T (bf16, fp32 accumulation; the two GEMMs are the MFMA
+// kernel below).  Projections and norms are left out.
 #include <chrono>
 #include <vector>
 
@@ -68,6 +66,253 @@ __global__ __launch_bounds__(256) void swiglu_kernel(const __bf16* __restrict__ 
     }
 }
 
+// ---- the FFN's GEMMs ------------------------------------------------------
+// C[M][N] = A[M][K] . Wt[N][K]^T with bf16 inputs, fp32 accumulation and a bf16
+// (round-to-nearest-even) result: the shape of a decode batch's projections,
+// M (requests) small and N, K model widths, so the weight rows dominate the
+// traffic.  A workgroup of kGemmWaves waves owns 16 * NT output columns and
+// 16 * MT rows.  Its waves split K: wave w takes kGemmUnroll consecutive
+// 32-element steps at a time (every weight row is read in 256-byte runs), all
+// their loads in flight before the products.  Per step a lane loads 16
+// contiguous bytes of one weight row per column tile (B operand: column =
+// lane % 16, k = 8 * (lane / 16) ...) and of one activation row per row tile
+// (A operand), and v_mfma_f32_16x16x32_bf16 accumulates each 16 x 16 tile
+// (lane holds rows 4 * (lane / 16) + v, column lane % 16).  Weights are loaded
+// non-temporally: they are read once, and the activations (read by every
+// workgroup) then stay in L2.  The waves' partial tiles are summed in LDS.
+// K must be a multiple of 8 and rows 16-byte aligned.
+constexpr int kGemmWaves = 8;
+
+template <int MT, int NT, int U>
+__global__ __launch_bounds__(kGemmWaves * kWave) void ffn_gemm_kernel(const __bf16* __restrict__ A,
+                                                                      const __bf16* __restrict__ Wt,
+                                                                      __bf16* __restrict__ C, int32_t M, int32_t N,
+                                                                      int32_t K) {
+    __shared__ float red[kGemmWaves][NT][MT][4][kWave];
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int col = lane & 15, grp = lane >> 4;
+    const int n0 = blockIdx.x * 16 * NT, m0 = blockIdx.y * 16 * MT;
+    const __bf16* wrow[NT];
+    bool n_ok[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int n = n0 + 16 * nt + col;
+        n_ok[nt] = n < N;
+        wrow[nt] = Wt + (size_t)(n_ok[nt] ? n : 0) * K + grp * 8;
+    }
+    const __bf16* arow[MT];
+    bool m_ok[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = m0 + 16 * mt + col;
+        m_ok[mt] = m < M;
+        arow[mt] = A + (size_t)(m_ok[mt] ? m : 0) * K + grp * 8;
+    }
+    const u32x4 zero = {0, 0, 0, 0};
+    f32x4 acc[NT][MT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int steps = (K + 31) / 32;
+    for (int sb = wave * U; sb < steps; sb += kGemmWaves * U) {
+        u32x4 b[U][NT], a[U][MT];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = (sb + u) * 32;  // this lane's 8 elements start at k + 8 * grp
+            const bool k_ok = k + grp * 8 < K;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                b[u][nt] = (k_ok && n_ok[nt])
+                               ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow[nt] + k))
+                               : zero;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                a[u][mt] = (k_ok && m_ok[mt]) ? *reinterpret_cast<const u32x4*>(arow[mt] + k) : zero;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a[u][mt]),
+                                                                          __builtin_bit_cast(bf16x8, b[u][nt]),
+                                                                          acc[nt][mt], 0, 0, 0);
+    }
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) red[wave][nt][mt][v][lane] = acc[nt][mt][v];
+    __syncthreads();
+    for (int o = tid; o < 16 * MT * 16 * NT; o += kGemmWaves * kWave) {
+        const int ml = o / (16 * NT), nl = o % (16 * NT);  // row of the workgroup's rows, column of its columns
+        const int mt = ml / 16, i = ml % 16, nt = nl / 16;
+        const int v = i % 4, src = (i / 4) * 16 + nl % 16;
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < kGemmWaves; ++w) sum += red[w][nt][mt][v][src];
+        const int m = m0 + ml, n = n0 + nl;
+        if (m < M && n < N) C[(size_t)m * N + n] = (__bf16)sum;
+    }
+}
+
+// The same product for wide outputs (many column tiles), with the activations shared
+// through LDS: a workgroup's 8 waves are CG = 8 / KG column groups of 16 * NT
+// columns times KG K-groups.  K advances in chunks of KC = KG * U * 32 elements;
+// each chunk of the workgroup's 16 * MT activation rows is staged once in LDS
+// (double-buffered, rows padded by 16 bytes against bank conflicts) and read by
+// all column groups, while every wave prefetches its weights of the next chunk.
+// The K-groups' partial tiles are summed in LDS at the end.
+template <int MT, int NT, int KG, int U>
+__global__ __launch_bounds__(kGemmWaves * kWave) void ffn_gemm_lds_kernel(const __bf16* __restrict__ A,
+                                                                          const __bf16* __restrict__ Wt,
+                                                                          __bf16* __restrict__ C, int32_t M,
+                                                                          int32_t N, int32_t K) {
+    constexpr int CG = kGemmWaves / KG;
+    constexpr int KC = KG * U * 32;    // K elements per chunk
+    constexpr int ROWS = 16 * MT;
+    constexpr int PITCH = KC + 8;      // elements per staged row
+    constexpr int PIECES = ROWS * KC / 8;  // 16-byte pieces of a chunk
+    constexpr int kThreads = kGemmWaves * kWave;
+    constexpr int kStageBytes = 2 * ROWS * PITCH * 2;
+    constexpr int kRedBytes = KG * CG * NT * MT * 4 * kWave * 4;
+    static_assert(PIECES % kThreads == 0, "a chunk is an exact number of pieces per thread");
+    __shared__ __align__(16) uint8_t smem[kStageBytes > kRedBytes ? kStageBytes : kRedBytes];
+    uint16_t(*sa)[ROWS][PITCH] = reinterpret_cast<uint16_t(*)[ROWS][PITCH]>(smem);
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int col = lane & 15, grp = lane >> 4;
+    const int cg = wave % CG, kg = wave / CG;
+    const int n0 = blockIdx.x * 16 * NT * CG + cg * 16 * NT, m0 = blockIdx.y * ROWS;
+    const __bf16* wrow[NT];
+    bool n_ok[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+        const int n = n0 + 16 * nt + col;
+        n_ok[nt] = n < N;
+        wrow[nt] = Wt + (size_t)(n_ok[nt] ? n : 0) * K + grp * 8;
+    }
+    const u32x4 zero = {0, 0, 0, 0};
+    // this thread's pieces of an activation chunk: row, element offset
+    auto stage_load = [&](int k0, u32x4 (&ra)[PIECES / kThreads]) {
+#pragma unroll
+        for (int i = 0; i < PIECES / kThreads; ++i) {
+            const int pc = tid + i * kThreads;
+            const int row = pc / (KC / 8), kk = (pc % (KC / 8)) * 8;
+            const int m = m0 + row, k = k0 + kk;
+            ra[i] = (m < M && k < K) ? *reinterpret_cast<const u32x4*>(A + (size_t)m * K + k) : zero;
+        }
+    };
+    auto stage_store = [&](int buf, const u32x4 (&ra)[PIECES / kThreads]) {
+#pragma unroll
+        for (int i = 0; i < PIECES / kThreads; ++i) {
+            const int pc = tid + i * kThreads;
+            const int row = pc / (KC / 8), kk = (pc % (KC / 8)) * 8;
+            *reinterpret_cast<u32x4*>(&sa[buf][row][kk]) = ra[i];
+        }
+    };
+    auto load_w = [&](int k0, u32x4 (&b)[U][NT]) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int k = k0 + (kg * U + u) * 32;  // this lane's 8 elements start at k + 8 * grp
+            const bool k_ok = k + grp * 8 < K;
+#pragma unroll
+            for (int nt = 0; nt < NT; ++nt)
+                b[u][nt] = (k_ok && n_ok[nt])
+                               ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wrow[nt] + k))
+                               : zero;
+        }
+    };
+    f32x4 acc[NT][MT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int n_chunks = (K + KC - 1) / KC;
+    u32x4 ra[PIECES / kThreads], b[U][NT], bn[U][NT];
+    stage_load(0, ra);
+    load_w(0, b);
+    stage_store(0, ra);
+    __syncthreads();
+    for (int it = 0; it < n_chunks; ++it) {
+        const bool more = it + 1 < n_chunks;
+        if (more) {  // next chunk's weights and activations in flight during this chunk's products
+            load_w((it + 1) * KC, bn);
+            stage_load((it + 1) * KC, ra);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) {
+                const u32x4 af = *reinterpret_cast<const u32x4*>(&sa[it & 1][16 * mt + col][(kg * U + u) * 32 + grp * 8]);
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt)
+                    acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af),
+                                                                          __builtin_bit_cast(bf16x8, b[u][nt]),
+                                                                          acc[nt][mt], 0, 0, 0);
+            }
+        if (more) stage_store((it + 1) & 1, ra);
+        __syncthreads();
+        if (more) {
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int nt = 0; nt < NT; ++nt) b[u][nt] = bn[u][nt];
+        }
+    }
+    // the staging buffers are free now (the loop ended with a barrier): K-group partials
+    float(*red)[CG][NT][MT][4][kWave] = reinterpret_cast<float(*)[CG][NT][MT][4][kWave]>(smem);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) red[kg][cg][nt][mt][v][lane] = acc[nt][mt][v];
+    __syncthreads();
+    constexpr int COLS = 16 * NT * CG;
+    const int nb = blockIdx.x * COLS;
+    for (int o = tid; o < ROWS * COLS; o += kThreads) {
+        const int ml = o / COLS, nl = o % COLS;  // row of the workgroup's rows, column of its columns
+        const int g = nl / (16 * NT), nt = (nl / 16) % NT, mt = ml / 16, i = ml % 16;
+        const int v = i % 4, src = (i / 4) * 16 + nl % 16;
+        float sum = 0.f;
+#pragma unroll
+        for (int w = 0; w < KG; ++w) sum += red[w][g][nt][mt][v][src];
+        const int m = m0 + ml, n = nb + nl;
+        if (m < M && n < N) C[(size_t)m * N + n] = (__bf16)sum;
+    }
+}
+
+// Wide outputs (N >= 16384: at least 256 workgroups of 64 columns) with at most 32 rows use
+// the LDS kernel with 4 column groups of 16 columns x 2 K-groups (measured on 32 x 4096 x 28672:
+// 58.9 us, against 64.0 with 128 columns per workgroup and 60.1 with 8 column groups and one
+// K-group); the others the direct kernel with 16 columns per workgroup (enough workgroups for
+// narrow outputs: 48 us on 32 x 14336 x 4096, 66 with 32 columns).
+static hipError_t launch_ffn_gemm(const void* A, const void* Wt, void* C, int32_t M, int32_t N, int32_t K,
+                                  hipStream_t st) {
+    const __bf16* a = (const __bf16*)A;
+    const __bf16* w = (const __bf16*)Wt;
+    __bf16* c = (__bf16*)C;
+    const dim3 block(kGemmWaves * kWave);
+    if (N >= 16384 && M <= 32) {
+        constexpr int CG = 4, NT = 1;
+        const dim3 grid((unsigned)((N + 16 * NT * CG - 1) / (16 * NT * CG)), (unsigned)((M + 31) / 32));
+        hipLaunchKernelGGL((ffn_gemm_lds_kernel<2, NT, kGemmWaves / CG, 4>), grid, block, 0, st, a, w, c, M, N, K);
+    } else if (M <= 16) {
+        hipLaunchKernelGGL((ffn_gemm_kernel<1, 1, 4>), dim3((unsigned)((N + 15) / 16), (unsigned)((M + 15) / 16)),
+                           block, 0, st, a, w, c, M, N, K);
+    } else if (M <= 32) {
+        hipLaunchKernelGGL((ffn_gemm_kernel<2, 1, 4>), dim3((unsigned)((N + 15) / 16), (unsigned)((M + 31) / 32)),
+                           block, 0, st, a, w, c, M, N, K);
+    } else {
+        hipLaunchKernelGGL((ffn_gemm_kernel<4, 1, 4>), dim3((unsigned)((N + 15) / 16), (unsigned)((M + 63) / 64)),
+                           block, 0, st, a, w, c, M, N, K);
+    }
+    return hipGetLastError();
+}
+
 // The gather kernel copies from one XCD while normal-batch layers run: the link rate
 // holds and the other XCDs keep serving HBM (from all XCDs, the concurrent layers
 // would barely progress until the recall ends).
@@ -84,7 +329,6 @@ using namespace pulse;
 
 struct pulse_irq {
     hipStream_t cmp = nullptr, io = nullptr;
-    rocblas_handle blas = nullptr;
     int64_t* flag_host = nullptr;  // pinned, host-mapped
     int64_t* flag_dev = nullptr;
     int64_t seq = 0;
@@ -110,6 +354,10 @@ static pulse_status check_normal(const pulse_normal_layer* n) {
                       n->w_gate_up && n->w_down && n->x && n->gu && n->h && n->y && n->dev_status,
                   PULSE_ERR_INVALID_ARG);
     PULSE_REQUIRE(n->ws && n->ws_bytes >= ws_layout(n->shape, n->B, n->k_max, 0).total, PULSE_ERR_WORKSPACE);
+    // the FFN GEMMs load 16-byte pieces of rows of length D and d_ff
+    PULSE_REQUIRE(n->d_ff % 8 == 0, PULSE_ERR_UNSUPPORTED);
+    for (const void* p : {n->w_gate_up, n->w_down, (const void*)n->x, (const void*)n->h})
+        PULSE_REQUIRE(((uintptr_t)p & 15) == 0, PULSE_ERR_INVALID_ARG);
     return PULSE_OK;
 }
 
@@ -127,22 +375,13 @@ static pulse_status normal_layer(pulse_irq* irq, const pulse_normal_layer& n, hi
     const int64_t nx = (int64_t)B * D;
     hipLaunchKernelGGL(to_bf16_kernel, dim3(grid_for(nx)), dim3(256), 0, hs, n.out, (__bf16*)n.x, nx);
     if (hipGetLastError() != hipSuccess) return PULSE_ERR_HIP;
-    const float one = 1.f, zero = 0.f;
-    // [B][2F] = x [B][D] . W_gu^T   (column-major: (2F x B) = W_gu^T(2F x D) . x^T(D x B))
-    if (rocblas_gemm_ex(irq->blas, rocblas_operation_transpose, rocblas_operation_none, 2 * F, B, D, &one,
-                        n.w_gate_up, rocblas_datatype_bf16_r, D, n.x, rocblas_datatype_bf16_r, D, &zero, n.gu,
-                        rocblas_datatype_bf16_r, 2 * F, n.gu, rocblas_datatype_bf16_r, 2 * F, rocblas_datatype_f32_r,
-                        rocblas_gemm_algo_standard, 0, 0) != rocblas_status_success)
-        return PULSE_ERR_HIP;
+    // gu [B][2F] = x [B][D] . W_gu^T
+    if (launch_ffn_gemm(n.x, n.w_gate_up, n.gu, B, 2 * F, D, hs) != hipSuccess) return PULSE_ERR_HIP;
     hipLaunchKernelGGL(swiglu_kernel, dim3(grid_for((int64_t)B * F)), dim3(256), 0, hs, (const __bf16*)n.gu,
                        (__bf16*)n.h, B, F);
     if (hipGetLastError() != hipSuccess) return PULSE_ERR_HIP;
-    // [B][D] = h [B][F] . W_down^T
-    if (rocblas_gemm_ex(irq->blas, rocblas_operation_transpose, rocblas_operation_none, D, B, F, &one, n.w_down,
-                        rocblas_datatype_bf16_r, F, n.h, rocblas_datatype_bf16_r, F, &zero, n.y,
-                        rocblas_datatype_bf16_r, D, n.y, rocblas_datatype_bf16_r, D, rocblas_datatype_f32_r,
-                        rocblas_gemm_algo_standard, 0, 0) != rocblas_status_success)
-        return PULSE_ERR_HIP;
+    // y [B][D] = h [B][F] . W_down^T
+    if (launch_ffn_gemm(n.h, n.w_down, n.y, B, D, F, hs) != hipSuccess) return PULSE_ERR_HIP;
     if (hipEventRecord(ev_end, hs) != hipSuccess) return PULSE_ERR_HIP;
     return PULSE_OK;
 }
@@ -161,8 +400,6 @@ pulse_status pulse_irq_create(pulse_stream_t compute_stream, pulse_stream_t io_s
         *irq->flag_host = 0;
         fail = hipHostGetDevicePointer((void**)&irq->flag_dev, irq->flag_host, 0) != hipSuccess;
     }
-    fail = fail || rocblas_create_handle(&irq->blas) != rocblas_status_success;
-    fail = fail || rocblas_set_stream(irq->blas, irq->cmp) != rocblas_status_success;
     if (fail) {
         pulse_irq_destroy(irq);
         return PULSE_ERR_HIP;
@@ -176,7 +413,6 @@ pulse_status pulse_irq_destroy(pulse_irq* irq) {
     if (irq->cmp) (void)hipStreamSynchronize(irq->cmp);
     if (irq->io) (void)hipStreamSynchronize(irq->io);
     for (hipEvent_t e : irq->events) (void)hipEventDestroy(e);
-    if (irq->blas) (void)rocblas_destroy_handle(irq->blas);
     if (irq->flag_host) (void)hipHostFree(irq->flag_host);
     delete irq;
     return PULSE_OK;

@@ -76,9 +76,19 @@ def test_irq_mode_matches_chained(setup, mode, use_engine):
     assert (stats["mean_recall_us"] > 0) != use_engine
 
 
-def test_normal_layers_compute_attention_and_ffn(setup):
+@pytest.mark.parametrize("shape", ["b4_ff512", "b37_ff1000", "b20_ff8200_hq9"])
+def test_normal_layers_compute_attention_and_ffn(setup, shape):
+    """The normal batch's attention and SwiGLU FFN (the library's MFMA GEMMs) against fp32
+    references: 4 requests with d_ff 512; 37 requests with d_ff 1000 (a partial tile of rows,
+    of the gate/up columns and of the last 32-element step of K); 20 requests, 9 / 3 heads
+    (D = 1152) and d_ff 8200, whose 16400 gate/up columns take the LDS-staged kernel with a
+    partial K chunk, a partial 128-column workgroup and partial rows."""
     ml, ref, normal, sched, _ = setup
-    say("\n[gpu] irq normal batch numerics")
+    say(f"\n[gpu] irq normal batch numerics {shape}")
+    if shape == "b37_ff1000":
+        normal = NormalBatch(B=37, ctx=300, n_layers=N_NORM, d_ff=1000, seed=9)
+    elif shape == "b20_ff8200_hq9":
+        normal = NormalBatch(B=20, ctx=200, n_layers=N_NORM, d_ff=8200, Hq=9, Hkv=3, seed=10)
     ml.reset()
     torch.cuda.synchronize()
     stats, _ = ml.run_irq(sched, normal, mode="blocking")  # one normal layer per offload layer: all 3 run
@@ -87,7 +97,7 @@ def test_normal_layers_compute_attention_and_ffn(setup):
     for li, b in enumerate(normal.bufs):
         # attention over every resident token, fp32 reference
         B, Hq, d = b["q"].shape
-        Hkv, bs, n = 8, 16, normal.n_blocks
+        Hkv, bs, n = normal.shape.num_kv_heads, normal.shape.block_size, normal.n_blocks
         pool = b["pool"].view(torch.bfloat16).float().cpu().reshape(B, n, 2, Hkv, -1)
         K = pool[:, :, 0].reshape(B, n, Hkv, bs, d).permute(0, 2, 1, 3, 4).reshape(B, Hkv, n * bs, d)
         V = pool[:, :, 1].reshape(B, n, Hkv, d, bs).permute(0, 2, 1, 4, 3).reshape(B, Hkv, n * bs, d)
@@ -110,3 +120,18 @@ def test_irq_rejects_bad_arguments(setup):
         sched.step([], normal.layers)
     with pytest.raises(P.PulseError):
         sched.step([ml.layers[0].layer_args()], normal.layers, mode=7)
+    # the FFN GEMMs need d_ff % 8 == 0 and 16-byte aligned rows; rejected before any work
+    L = normal.layers[0]
+    d_ff, w_down = L.d_ff, L.w_down
+    try:
+        L.d_ff = 1001
+        with pytest.raises(P.PulseError) as e:
+            sched.step([ml.layers[0].layer_args()], [L])
+        assert e.value.status == P.PULSE_ERR_UNSUPPORTED
+        L.d_ff = d_ff
+        L.w_down = w_down + 2
+        with pytest.raises(P.PulseError) as e:
+            sched.step([ml.layers[0].layer_args()], [L])
+        assert e.value.status == P.PULSE_ERR_INVALID_ARG
+    finally:
+        L.d_ff, L.w_down = d_ff, w_down
