@@ -30,6 +30,15 @@ def test_library_exports_every_declared_symbol():
     assert set(P.EXPORTED) == set(decl)
 
 
+def test_library_needs_only_the_hip_runtime():
+    """libpulse.so links no BLAS or other ROCm library: every kernel, the normal batch's FFN
+    GEMMs included, is built into it, so it loads wherever the HIP runtime does."""
+    out = subprocess.run(["readelf", "-d", P.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    needed = re.findall(r"\(NEEDED\)\s+Shared library: \[([^\]]+)\]", out)
+    rocm = [n for n in needed if not re.match(r"lib(c|m|dl|gcc_s|stdc\+\+|pthread|rt)\.so", n)]
+    assert rocm and all(n.startswith("libamdhip64.so") for n in rocm), needed
+
+
 def test_status_strings():
     for code, name in [(0, "PULSE_OK"), (4, "PULSE_ERR_POOL_EXHAUSTED"), (7, "PULSE_ERR_BAD_INDEX")]:
         assert P.status_string(code) == name
