@@ -25,8 +25,10 @@
 // workgroup per (r, h) it writes the result directly.  Otherwise each workgroup writes one partial (m, l, O) to
 // the workspace and a combine kernel merges those few partials, one thread
 // per output element, with independent loads.  (Merging in the last workgroup
-// to finish would need a device-scope release fence per workgroup, which on
-// gfx950 writes back the XCD's L2 and costs more than the extra launch.)
+// to finish instead needs a device-scope release per workgroup, an L2
+// write-back on gfx950 measured at about 9 ns per workgroup, plus a merge on
+// the kernel's tail and counters that start at zero in the workspace: it would
+// save well under the combine launch's 3.6 us.)
 #include "pulse_internal.h"
 
 namespace pulse {
