@@ -58,10 +58,10 @@ def assert_selection_ok(w, gidx, gcnt, oidx, ocnt, oscores):
     return n_ties
 
 
-def oracle_recall(w, idx, cnt, free_slots=None, free_head=0):
-    """The oracle's recall of selection (idx, cnt) from the workload's initial table and pool;
-    free_slots / free_head default to the workload's free list and 0."""
-    table = w.table0.copy()
+def oracle_recall(w, idx, cnt, free_slots=None, free_head=0, table0=None):
+    """The oracle's recall of selection (idx, cnt) from the workload's initial table (or table0)
+    and pool; free_slots / free_head default to the workload's free list and 0."""
+    table = (w.table0 if table0 is None else table0).copy()
     pool = W.initial_pool(w).view(np.uint8).reshape(w.n_slots, -1).copy()
     host = w.kv.view(np.uint8).reshape(w.total_blocks, -1)
     free = w.free_slots if free_slots is None else free_slots

@@ -181,6 +181,31 @@ def test_select_overflow_reports_and_empties_request():
     assert gcnt[1] == 0 and np.all(gidx[1] == -1) and gcnt[0] == 14
 
 
+def test_chained_layer_with_overflowing_request():
+    """pulse_decode_layer when one request's selection exceeds k_max: SELECT_OVERFLOW, that
+    request's selection is empty (attention out 0, lse -inf), and the other requests are
+    selected, recalled and attended exactly as the oracle does on the same inputs."""
+    spec, s = W.custom("ovfc", [900, 1500, 700], Hq=32, Hkv=8, bs=16, k_mid=[6, 40, 4], n_sink=1, n_local=8,
+                       resident_frac=0.1, heavy_per_req=4)
+    w, st = build(spec, s, k_max=24)
+    st.reset()
+    st.decode_layer()
+    torch.cuda.synchronize()
+    assert st.status() == P.PULSE_ERR_SELECT_OVERFLOW
+    dig = st.digests.cpu().numpy().view(np.uint16)[: w.total_blocks]
+    gidx, gcnt = st.selection()
+    rc, oidx, ocnt, osc = oracle_selection(w, dig, k_max=st.k_max)
+    assert rc == O.ERR_SELECT_OVERFLOW and ocnt[1] == 0 and gcnt[1] == 0 and np.all(gidx[1] == -1)
+    assert_selection_ok(w, gidx, gcnt, oidx, ocnt, osc)
+    rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt)
+    assert rc == 0 and stats[0] > 0
+    assert_recall_equal(st, table, pool, fh, stats)
+    out, lse = oracle_attention(w, pool, table, gidx, gcnt)
+    assert np.all(out[1] == 0) and np.all(np.isneginf(lse[1]))
+    err = assert_attention_close(st, out, lse)
+    say(f"  stats={stats} attn_err={err[0]:.1e}")
+
+
 # ------------------------------------------------------------------ recall
 
 RECALL_CASES = [
@@ -223,6 +248,10 @@ def test_recall_pool_exhaustion_leaves_state():
     assert torch.equal(st.table, st.table0) and int(st.free_head.item()) == 0 and torch.equal(st.pool, pool0)
     n_missing, _, nbytes = st.recall_stats()
     assert n_missing > 10 and nbytes == 0
+    gidx, gcnt = st.selection()
+    rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt)  # statistics as the oracle's, exactly
+    assert rc == O.ERR_POOL_EXHAUSTED
+    assert_recall_equal(st, table, pool, fh, stats)
 
 
 def test_recall_rejects_unsorted_and_out_of_range():
@@ -250,17 +279,18 @@ def test_recall_rejects_unsorted_and_out_of_range():
     assert_recall_equal(st, table, pool, fh, stats)
 
 
-BAD_FREE = ["slot_past_pool", "negative_slot", "head_past_list", "bad_slot_past_range"]
+BAD_FREE = ["slot_past_pool", "negative_slot", "head_past_list", "bad_slot_past_range", "table_entry_past_pool"]
 
 
 @pytest.mark.parametrize("bad", BAD_FREE)
 @pytest.mark.parametrize("path", ["recall_gather", "decode_layer", "engine"])
 def test_recall_rejects_bad_free_slot(path, bad):
-    """A free list whose entries in the range the recall takes lie outside the pool, or a
-    free-list head outside the list: BAD_INDEX, and table, free head, statistics and every
-    pool byte exactly as the oracle leaves them (nothing written, bytes 0).  A bad entry
-    past that range is never read.  Afterwards a clean recall on the same state matches the
-    oracle.  Covers the standalone recall, the chained layer-step and the paper's engine."""
+    """A free list whose entries in the range the recall takes lie outside the pool, a
+    free-list head outside the list, or a selected block whose table entry lies past the pool:
+    BAD_INDEX, and table, free head, statistics and every pool byte exactly as the oracle
+    leaves them (nothing written, bytes 0).  A bad entry past the free-list range is never
+    read.  Afterwards a clean recall on the same state matches the oracle.  Covers the
+    standalone recall, the chained layer-step and the paper's engine."""
     spec, s = W.custom("badfree", [3000, 2000, 700], Hq=32, Hkv=8, bs=16, k_mid=40, n_sink=1, n_local=8,
                        resident_frac=0.05, heavy_per_req=10)
     w, st = build(spec, s)
@@ -273,8 +303,10 @@ def test_recall_rejects_bad_free_slot(path, bad):
         rc0, _, _, _, clean = oracle_recall(w, gidx, gcnt)
         n_miss = clean[0]
         assert rc0 == 0 and n_miss >= 3 and n_miss < w.free_slots.size
-        free, fh0 = w.free_slots.copy(), 0
-        if bad == "slot_past_pool":
+        free, fh0, table0 = w.free_slots.copy(), 0, w.table0.copy()
+        if bad == "table_entry_past_pool":
+            table0[1, 0] = w.n_slots  # request 1's sink block: always selected
+        elif bad == "slot_past_pool":
             free[n_miss - 1] = w.n_slots  # the last slot the recall takes
         elif bad == "negative_slot":
             free[n_miss // 2] = -3
@@ -285,6 +317,7 @@ def test_recall_rejects_bad_free_slot(path, bad):
         st.reset()
         st.free_slots.copy_(torch.from_numpy(free))
         st.free_head.fill_(fh0)
+        st.table.copy_(torch.from_numpy(table0))
         pool0 = st.pool.clone()
 
         def run():
@@ -302,7 +335,7 @@ def test_recall_rejects_bad_free_slot(path, bad):
 
         run()
         gidx, gcnt = st.selection()
-        rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt, free_slots=free, free_head=fh0)
+        rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt, free_slots=free, free_head=fh0, table0=table0)
         say(f"  {path}/{bad}: oracle rc={rc} stats={stats}; gpu status={st.status()} stats={st.recall_stats()}")
         if bad == "bad_slot_past_range":
             assert rc == 0 and st.status() == 0
@@ -310,11 +343,12 @@ def test_recall_rejects_bad_free_slot(path, bad):
             return
         assert rc == O.ERR_BAD_INDEX and stats[2] == 0
         assert st.status() == P.PULSE_ERR_BAD_INDEX
-        assert torch.equal(st.table, st.table0) and torch.equal(st.pool, pool0)
+        assert np.array_equal(st.table_np(), table0) and torch.equal(st.pool, pool0)
         assert_recall_equal(st, table, pool, fh, stats)
         # nothing changed: a clean recall of the same selection on this state matches the oracle
         st.free_slots.copy_(torch.from_numpy(w.free_slots))
         st.free_head.fill_(0)
+        st.table.copy_(st.table0)
         st.dev_status.zero_()
         run()
         assert st.status() == 0
@@ -541,5 +575,9 @@ def test_gather_scatter_engine_pool_exhaustion():
         torch.cuda.synchronize()
         assert st.status() == P.PULSE_ERR_POOL_EXHAUSTED
         assert torch.equal(st.table, st.table0) and int(st.free_head.item()) == 0 and torch.equal(st.pool, pool0)
+        gidx, gcnt = st.selection()
+        rc, table, pool, fh, stats = oracle_recall(w, gidx, gcnt)
+        assert rc == O.ERR_POOL_EXHAUSTED
+        assert_recall_equal(st, table, pool, fh, stats)
     finally:
         eng.destroy()
