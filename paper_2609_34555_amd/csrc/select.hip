@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     const int32_t* __restrict__ free_head, int32_t* __restrict__ miss_list, int32_t* __restrict__ miss_cnt,
     int32_t* __restrict__ run_cnt, int32_t* __restrict__ req_err, int32_t* __restrict__ misc, int32_t* status) {
     __shared__ __align__(16) uint32_t skey[kKeyCache];  // key of block j at [j] (cached path)
-    __shared__ uint32_t hist[256];
+    __shared__ uint32_t hist[2][256];  // radix histograms: one counted while the other is cleared
     __shared__ uint32_t sh_prefix, sh_kk;
     __shared__ bool sh_whole;
     __shared__ uint32_t wc[kSelWaves][2];
@@ -184,6 +184,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     // is above T, or equal to T and fewer than need_eq equal ones precede it.
     // All keys equal: T_mask = 0, so every key is "equal" and the first k are taken.
     uint32_t key_base = 0, T = 0, T_mask = 0, need_eq = (uint32_t)k;
+    // the radix select ended on a bucket taken whole: every key equal to T (masked) is chosen
+    bool eq_all_taken = false;
     // cached path: keys of blocks tid + 1024u in registers, mid_l = those that are middle
     uint32_t kreg[kPerThread];
     uint32_t mid_l = 0;
@@ -221,6 +223,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         kmin = last_lane(wave_scan(kmin, 0xFFFFFFFFu, OpMin()));
         kmax = last_lane(wave_scan(kmax, 0u, OpMax()));
         if (lane == 0) { wc[wid][0] = kmin; wc[wid][1] = kmax; }
+        if (tid < 256) hist[0][tid] = 0;  // the first radix pass's histogram
         __syncthreads();
         kmin = 0xFFFFFFFFu;
         kmax = 0u;
@@ -236,22 +239,21 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
             uint32_t mask = top >= 31 ? 0u : ~((2u << top) - 1u);  // offset bits already decided
             uint32_t prefix = 0u;                                    // their value
             uint32_t kk = (uint32_t)k;
-            for (int shift = top - 7;; shift -= 8) {
+            for (int shift = top - 7, pass = 0;; shift -= 8, ++pass) {
                 const int sh = shift > 0 ? shift : 0;
                 const uint32_t dmask = shift >= 0 ? 255u : (255u >> -shift);
-                if (tid < 256) hist[tid] = 0;
-                __syncthreads();
+                uint32_t* hcur = hist[pass & 1];  // cleared before the barrier that ended the last pass
                 if (cached) {
 #pragma unroll
                     for (int u = 0; u < kPerThread; ++u) {
                         if (u * kSelThreads >= n) break;
                         const uint32_t off = kreg[u] - kmin;
-                        if (((mid_l >> u) & 1u) && (off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
+                        if (((mid_l >> u) & 1u) && (off & mask) == prefix) atomicAdd(&hcur[(off >> sh) & dmask], 1u);
                     }
                 } else {
                     for (int64_t j = lo + tid; j < hi; j += kSelThreads) {
                         const uint32_t off = key32(rsc[j]) - kmin;
-                        if ((off & mask) == prefix) atomicAdd(&hist[(off >> sh) & dmask], 1u);
+                        if ((off & mask) == prefix) atomicAdd(&hcur[(off >> sh) & dmask], 1u);
                     }
                 }
                 __syncthreads();
@@ -260,7 +262,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                     // above(d) < kk <= above(d) + hist[d], above(d) = #offsets with digit > d.
                     uint32_t c[4];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) c[i] = hist[4 * lane + i];
+                    for (int i = 0; i < 4; ++i) c[i] = hcur[4 * lane + i];
                     const uint32_t sum = c[0] + c[1] + c[2] + c[3];
                     const uint32_t incl = wave_scan(sum, 0u, OpAdd());
                     uint32_t above = last_lane(incl) - incl;  // offsets in lanes above this one
@@ -273,6 +275,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
                         }
                         above += c[i];
                     }
+                } else if (tid < kWave + 256) {
+                    hist[(pass + 1) & 1][tid - kWave] = 0;  // the next pass's histogram
                 }
                 __syncthreads();
                 prefix = sh_prefix;
@@ -283,6 +287,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
             T = prefix;
             T_mask = mask;
             need_eq = kk;
+            eq_all_taken = sh_whole;
         }
     }
 
@@ -294,6 +299,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     uint32_t eq_carry = 0, sel_carry = 0, miss_carry = 0, runs = 0, prev_bit = 0;
     int32_t my_err = 0;
     const bool thr = !all_mid && !none_mid;
+    const bool skip_eq = (!thr || eq_all_taken) && n <= (int64_t)kSelThreads * kPerThread;
     // bits u of [0, 8) with a <= j0 + u < b
     auto range_mask = [](int64_t a, int64_t b, int64_t j0) -> uint32_t {
         const int64_t a_rel = a - j0, b_rel = b - j0;
@@ -330,10 +336,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
             gt_m &= mid_m;
             eq_m &= mid_m;
         }
-        // scan 1: equal keys before this thread's blocks
-        uint32_t eq_tot;
-        const uint32_t eq_before = eq_carry + block_scan(__popc(eq_m), scan[0], eq_tot);
-        uint32_t take = need_eq > eq_before ? need_eq - eq_before : 0u;  // equal keys still taken
+        // scan 1: equal keys before this thread's blocks (the lowest-index tie rule).  Not
+        // needed when every equal key is taken (or none can occur) and the request is one
+        // super-tile: consecutive scans of a multi-tile request need it between them, as
+        // they reuse scan[1].
+        uint32_t eq_tot = 0, take = kPerThread;  // equal keys still taken
+        if (!skip_eq) {
+            const uint32_t eq_before = eq_carry + block_scan(__popc(eq_m), scan[0], eq_tot);
+            take = need_eq > eq_before ? need_eq - eq_before : 0u;
+        }
         uint32_t sel_m = forced_m | gt_m;
 #pragma unroll
         for (int u = 0; u < kPerThread; ++u)
