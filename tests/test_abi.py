@@ -30,6 +30,19 @@ def test_library_exports_every_declared_symbol():
     assert set(P.EXPORTED) == set(decl)
 
 
+def test_header_compiles_as_strict_c_and_cxx():
+    """include/pulse.h is a plain C header: it compiles as C99, C11 and C++17 with every warning
+    an error, and a C translation unit can take the address of every declared entry point."""
+    for lang, std in (("c", "c99"), ("c", "c11"), ("c++", "c++17")):
+        cc = "gcc" if lang == "c" else "g++"
+        subprocess.run([cc, f"-std={std}", "-Wall", "-Wextra", "-Werror", "-pedantic", "-fsyntax-only", "-x", lang,
+                        HEADER], check=True)
+    names = declared_symbols()
+    src = '#include "pulse.h"\n' + "".join(f"void* p{i} = (void*)&{n};\n" for i, n in enumerate(names))
+    subprocess.run(["gcc", "-std=c11", "-Wall", "-Werror", "-fsyntax-only", "-I", os.path.dirname(HEADER), "-x", "c",
+                    "-"], input=src, text=True, check=True)
+
+
 def test_library_needs_only_the_hip_runtime():
     """libpulse.so links no BLAS or other ROCm library: every kernel, the normal batch's FFN
     GEMMs included, is built into it, so it loads wherever the HIP runtime does."""
