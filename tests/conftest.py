@@ -23,4 +23,17 @@ def _built_artifacts():
 
     if not os.path.exists(pbuild.LIB):
         pbuild.build_library()
+    cbuild = _load_c_build()
+    if not os.path.exists(cbuild.EXE):
+        cbuild.build_c_tests()
     yield
+
+
+def _load_c_build():
+    """tests/c/build.py (the C-ABI test program's build), loaded by path."""
+    import importlib.util
+
+    spec = importlib.util.spec_from_file_location("pulse_c_test_build", os.path.join(ROOT, "tests", "c", "build.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
