@@ -78,13 +78,14 @@ __device__ inline typename Mfma<DT>::vec zero_vec() {
     return __builtin_bit_cast(typename Mfma<DT>::vec, u32x4{0, 0, 0, 0});
 }
 
-// Attention of one wave over entries [e0, e0 + ne) of request r, KV head h.
+// Attention of one wave over entries [e0, e0 + ne) of request r, KV head h;
+// j_lane is the selected block of entry e0 + lane (loaded by the caller).
 // Leaves the running max (log2 domain) and the lane-group-reduced sum for
 // query column `col` in m_run / l_run, and O rows g = 4*grp + v in acc.
 template <int DT, int BS>
 __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16_t* __restrict__ pool,
                                     int32_t n_slots, const int32_t* __restrict__ table, int32_t max_blocks,
-                                    const int32_t* __restrict__ sel_row, int ctx, int32_t Hq, int32_t Hkv, int32_t G,
+                                    int32_t j_lane, int ctx, int32_t Hq, int32_t Hkv, int32_t G,
                                     int r, int h, int e0, int ne, float scale_log2, int32_t* status, int lane,
                                     float& m_run, float& l_run, f32x4 (&acc)[8]) {
     using M = Mfma<DT>;
@@ -100,7 +101,7 @@ __device__ inline void attend_split(const uint16_t* __restrict__ q, const uint16
     const int64_t n_r = ((int64_t)ctx + BS - 1) / BS;
     int my_slot = -1, my_nv = 0;
     if (lane < ne) {
-        const int32_t j = sel_row[e0 + lane];
+        const int32_t j = j_lane;
         if (j >= 0 && j < n_r && j < max_blocks) {
             const int32_t sl = table[(size_t)r * max_blocks + j];
             if (sl >= 0 && sl < n_slots) {
@@ -244,6 +245,11 @@ __global__ __launch_bounds__(W * kWave) void attn_splitk_kernel(
     float* out_rh = out + ((size_t)r * Hq + (size_t)h * G) * kHeadDim;
     float* lse_rh = lse ? lse + (size_t)r * Hq + (size_t)h * G : nullptr;
 
+    // this wave's selected blocks (one per lane) are loaded with the count they
+    // depend on, not after it: one memory round trip fewer before the first K load
+    const int s = wg * W + wave;
+    const int e0 = s * eps;
+    const int32_t j_lane = (lane < eps && e0 + lane < k_max) ? sel_idx[(size_t)r * k_max + e0 + lane] : -1;
     int32_t cnt = sel_cnt[r];
     if (cnt < 0 || cnt > k_max) {
         if (tid == 0) report(status, PULSE_ERR_BAD_INDEX);
@@ -258,12 +264,10 @@ __global__ __launch_bounds__(W * kWave) void attn_splitk_kernel(
         }
         return;
     }
-    const int s = wg * W + wave;
-    const int e0 = s * eps;
     const int ne = min(e0 + eps, cnt) - e0;
     float m_run, l_run;
     f32x4 acc[8];
-    attend_split<DT, BS>(q, pool, n_slots, table, max_blocks, sel_idx + (size_t)r * k_max, ctx_len[r], Hq, Hkv, G, r,
+    attend_split<DT, BS>(q, pool, n_slots, table, max_blocks, j_lane, ctx_len[r], Hq, Hkv, G, r,
                          h, e0, ne, scale_log2, status, lane, m_run, l_run, acc);
     // wave partials to LDS
     if (grp == 0 && col < G) s_ml[wave * G + col] = make_float2(m_run, l_run);
