@@ -171,6 +171,50 @@ def test_select_duplicate_blocks_take_lowest_index():
         assert len(mid) == 7 and max(mid) < 50
 
 
+def test_equal_keys_across_two_tiles_chained():
+    """Every block of a 9000-block request holds the same keys, so every middle score is
+    equal: the first 8500 middle blocks in index order are taken, the equal keys ranked
+    across the selection pass's 8192-block tile boundary.  Only the forced blocks are
+    resident, so the recall plan is one run of 8500 blocks crossing that boundary;
+    selection, plan, pool and attention against the oracle."""
+    spec, s = W.custom("eq2t", [9000 * 16], Hq=32, Hkv=8, bs=16, dtype="bf16", k_mid=8500, n_sink=1, n_local=8,
+                       resident_frac=0.0, planted=False)
+    w, st = build(spec, s)
+    w.kv[1:] = w.kv[0]  # one block's keys and values everywhere, resident copies included
+    st.pool[: w.resident_blocks.size] = torch.from_numpy(w.kv[w.resident_blocks].view(np.int16)).cuda()
+    st.build_digests(w.solo_kv_head)
+    res = full_check(w, st, chained=True)
+    assert res["ties"] == 0 and res["stats"][0] == 8500 and res["stats"][1] == 1, res["stats"]
+    gidx, gcnt = st.selection()
+    assert gcnt[0] == 8509 and np.array_equal(gidx[0, :8501], np.arange(8501))
+
+
+def test_tied_keys_cut_across_two_tiles():
+    """201 exact copies of a request's best middle block straddle the 8192-block tile
+    boundary (blocks 8100 .. 8300) and only 150 places remain for them: the lowest-index
+    rule takes the first copies in block order, with the equal-key ranks of the first tile
+    carried into the second; both sides must pick the same blocks."""
+    spec, s = W.custom("tie2t", [9000 * 16], Hq=32, Hkv=8, bs=16, dtype="bf16", k_mid=151, n_sink=1, n_local=8,
+                       planted=False)
+    w, st = build(spec, s)
+    dig = O.build_digests(w.kv, w.blk_off, w.ctx_len, w.Hkv, w.bs, w.d, w.dtype_code, w.solo_kv_head)
+    sc = O.score(w.q, dig, w.blk_off, w.Hq, w.Hkv, w.d, w.dtype_code, w.solo_kv_head)
+    best = 1 + int(np.argmax(sc[1: 9000 - 8]))
+    src = w.kv[best].copy()
+    w.kv[8100:8301] = src
+    st.build_digests(w.solo_kv_head)
+    st.select()
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    dig = st.digests.cpu().numpy().view(np.uint16)[: w.total_blocks]
+    rc, oidx, ocnt, osc = oracle_selection(w, dig)
+    gidx, gcnt = st.selection()
+    assert rc == 0 and np.array_equal(gidx, oidx) and np.array_equal(gcnt, ocnt)
+    mid = [j for j in gidx[0, : gcnt[0]] if 1 <= j < 9000 - 8]
+    copies = [j for j in mid if 8100 <= j <= 8300]
+    assert len(mid) == 151 and copies[0] == 8100 and 8192 <= copies[-1] <= 8300
+
+
 def test_select_overflow_reports_and_empties_request():
     spec, s = W.custom("ovf", [800, 800], Hq=32, Hkv=8, bs=16, k_mid=[5, 30], n_sink=1, n_local=8)
     w, st = build(spec, s, k_max=20)
