@@ -69,7 +69,7 @@ SELECT_CASES = [
     ("k_zero", [400, 300], 32, 8, 16, "bf16", 0, 1, 8),
     ("forced_cover", [100, 40], 32, 8, 16, "bf16", 4, 3, 5),
     ("big_n", [131072, 70000], 32, 8, 16, "bf16", [247, 100], 1, 8),
-    # > 8192 middle blocks: keys re-read from L2 each radix pass, two ordered super-tiles
+    # > 8192 middle blocks: keys re-read from L2 each radix pass, two ordered tiles
     ("uncached_two_tiles", [150000, 140000, 3000], 32, 8, 16, "bf16", [300, 5, 40], 1, 8),
     # 100 / 140 / 60 / 100 blocks: the equal-length guess of the score and select kernels
     # (100 blocks each) holds for requests 0 and 3 and fails for 1 (length) and 2 (offset)
@@ -103,8 +103,8 @@ def test_select_parity(case):
 
 
 def test_chained_layer_beyond_key_cache():
-    """A chained layer-step whose requests exceed the select kernel's LDS key cache and its
-    first super-tile of prefetched table entries (plan mode reads the table in the kernel)."""
+    """A chained layer-step whose requests exceed the select kernel's one tile of keys held in
+    registers and its prefetched table entries (plan mode reads the rest of the table in the kernel)."""
     spec, s = W.custom("long", [150000, 9000], Hq=32, Hkv=8, bs=16, dtype="bf16", k_mid=[200, 30], n_sink=1,
                        n_local=8, resident_frac=0.1, heavy_per_req=6)
     w, st = build(spec, s)
