@@ -35,6 +35,7 @@ constexpr int kSelWaves = kSelThreads / kWave;
 constexpr int kRounds = 8;                          // rounds per tile
 constexpr int kTile = kRounds * kSelThreads;        // blocks per tile; one-tile requests keep keys in registers
 constexpr int kEntries = kRounds * kSelWaves;       // (round, wave) entries of a tile: two per lane
+constexpr int kWords = kRounds / 4;                 // words of per-round byte counts
 
 // Inclusive scan of x over the 64 lanes of a wave with `op`, in registers
 // (DPP row shifts within 16-lane rows, then row broadcasts of lanes 15 and
@@ -259,9 +260,9 @@ __device__ inline void select_request(SelLds& L, const float* rsc, const float (
         uint32_t take_m = eq_m;  // equal keys taken
         if (!skip_eq) {
             // the lowest-index tie rule: the rank of each equal key among the equal keys
-            uint32_t xe[2];
+            uint32_t xe[kWords];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < kWords; ++h) {
                 const uint32_t be = spread_bytes(eq_m >> (4 * h));
                 const uint32_t ie = wave_scan(be, 0u, OpAdd());
                 xe[h] = ie - be;
@@ -302,27 +303,23 @@ __device__ inline void select_request(SelLds& L, const float* rsc, const float (
         // (missing) lanes of every round.
         const uint32_t pm = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)miss_m, 0x138, 0xF, 0xF, false);  // wave_shr:1
         const uint32_t st_m = miss_m & ~pm;  // missing, the block before (in this wave's round) not
-        uint32_t xs[2], xm[2], ts[2], tm[2];
+        uint32_t xs[kWords], xm[kWords];
+        const uint32_t m_first = (uint32_t)__builtin_amdgcn_readlane((int)miss_m, 0);
+        const uint32_t m_last = (uint32_t)__builtin_amdgcn_readlane((int)miss_m, 63);
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < kWords; ++h) {
             const uint32_t bs = spread_bytes(sel_m >> (4 * h)), bm = spread_bytes(miss_m >> (4 * h));
             const uint32_t is = wave_scan(bs, 0u, OpAdd()), im = wave_scan(bm, 0u, OpAdd());
             xs[h] = is - bs;  // lanes below, per round
             xm[h] = im - bm;
-            ts[h] = last_lane(is);
-            tm[h] = last_lane(im);
-        }
-        const uint32_t tst0 = last_lane(wave_scan(spread_bytes(st_m), 0u, OpAdd()));
-        const uint32_t tst1 = last_lane(wave_scan(spread_bytes(st_m >> 4), 0u, OpAdd()));
-        const uint32_t m_first = (uint32_t)__builtin_amdgcn_readlane((int)miss_m, 0);
-        const uint32_t m_last = (uint32_t)__builtin_amdgcn_readlane((int)miss_m, 63);
-        if (lane < kRounds) {  // lane u writes this wave's entry of round u
-            const int h = lane >> 2, sh = 8 * (lane & 3);
-            const uint32_t c_sel = ((h ? ts[1] : ts[0]) >> sh) & 0xFFu, c_miss = ((h ? tm[1] : tm[0]) >> sh) & 0xFFu;
-            const uint32_t c_st = ((h ? tst1 : tst0) >> sh) & 0xFFu;
-            const int e = lane * kSelWaves + wid;
-            L.cnt[e] = c_sel | (c_miss << 16);
-            L.rb[e] = c_st | (((m_first >> lane) & 1u) << 8) | (((m_last >> lane) & 1u) << 9);
+            const uint32_t ts = last_lane(is), tm = last_lane(im);
+            const uint32_t tst = last_lane(wave_scan(spread_bytes(st_m >> (4 * h)), 0u, OpAdd()));
+            if (lane >= 4 * h && lane < 4 * h + 4) {  // lane u writes this wave's entry of round u
+                const int sh = 8 * (lane & 3);
+                const int e = lane * kSelWaves + wid;
+                L.cnt[e] = ((ts >> sh) & 0xFFu) | (((tm >> sh) & 0xFFu) << 16);
+                L.rb[e] = ((tst >> sh) & 0xFFu) | (((m_first >> lane) & 1u) << 8) | (((m_last >> lane) & 1u) << 9);
+            }
         }
         __syncthreads();
         const RowScan cs = row_scan(L.cnt, wid);
