@@ -17,10 +17,11 @@
 //      offsets with those bits equal to T that are taken;
 //   2. one ordered pass per tile: block j is chosen if its masked offset is
 //      above T, or equal to T and fewer than need_eq equal ones precede it
-//      (exactly the lowest-index tie rule).  Positions come from wave ballots
-//      (the rank of a lane among the chosen lanes of its wave) plus a prefix
-//      over the 128 (round, wave) counts of the tile, which every wave scans
-//      itself from LDS after one barrier.
+//      (exactly the lowest-index tie rule).  Positions come from per-round
+//      counts packed as bytes and summed by DPP wave scans (which give each
+//      lane its rank among the chosen lanes of its wave) plus a prefix over
+//      the 128 (round, wave) counts of the tile, which every wave scans itself
+//      from LDS after one barrier.
 // With a block table the same pass writes the recall plan: missing blocks
 // (table entry -1) in listed order, their count and their run count.
 // The select kernel is issue-bound on its compute unit (16 waves share 4
