@@ -330,7 +330,7 @@ def generate(spec: Spec, seed: int, *, kv_alloc: Optional[Callable] = None, thre
         with ThreadPoolExecutor(max_workers=nthreads) as ex:
             list(ex.map(lambda jb: _fill_chunk(kv[jb[0]:jb[1]], jb[2], dtype), jobs))
 
-    kv5 = kv.reshape(total, 2, Hkv, -1)
+    kv5 = kv.reshape(total, 2, Hkv, bs * d)
     # planting in the retrieval head's keys
     if spec.planted:
         qf = to_float(q, dtype).astype(np.float64)

@@ -63,7 +63,7 @@ def oracle_recall(w, idx, cnt, free_slots=None, free_head=0, table0=None):
     and pool; free_slots / free_head default to the workload's free list and 0."""
     table = (w.table0 if table0 is None else table0).copy()
     pool = W.initial_pool(w).view(np.uint8).reshape(w.n_slots, -1).copy()
-    host = w.kv.view(np.uint8).reshape(w.total_blocks, -1)
+    host = w.kv.view(np.uint8).reshape(w.total_blocks, 2 * w.elems_per_block)
     free = w.free_slots if free_slots is None else free_slots
     rc, fh, stats = O.recall(host, w.blk_off, idx, cnt, table, free, free_head, pool, w.unit_bytes)
     return rc, table, pool, fh, stats

@@ -215,6 +215,39 @@ def test_tied_keys_cut_across_two_tiles():
     assert len(mid) == 151 and copies[0] == 8100 and 8192 <= copies[-1] <= 8300
 
 
+def _random_case(seed):
+    """A seeded small workload: batch, ragged (and empty) contexts, block size, group size,
+    forced-block counts, budgets from 0 to past the middle, planted or not, free-list order."""
+    rng = np.random.default_rng([seed, 3107])
+    B = int(rng.integers(1, 7))
+    bs = int(rng.choice([16, 32, 64]))
+    Hkv = int(rng.choice([1, 2, 8]))
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    ctx = [0 if rng.random() < 0.1 else int(rng.integers(1, 24000)) for _ in range(B)]
+    n_max = max(1, max(-(-c // bs) for c in ctx))
+    k_mid = [int(rng.choice([0, int(rng.integers(1, 40)), int(rng.integers(1, n_max + 5))])) for _ in range(B)]
+    n_sink, n_local = int(rng.integers(0, 3)), int(rng.integers(0, 9))
+    spec, s = W.custom(f"rand{seed}", ctx, Hq=G * Hkv, Hkv=Hkv, bs=bs, dtype=str(rng.choice(["bf16", "f16"])),
+                       k_mid=k_mid, n_sink=n_sink, n_local=n_local, resident_frac=float(rng.choice([0.0, 0.1, 0.5])),
+                       heavy_per_req=int(rng.integers(0, 8)), planted=bool(rng.random() < 0.5),
+                       free_order=str(rng.choice(["ascending", "shuffled"])), seed=seed)
+    return spec, s
+
+
+@pytest.mark.parametrize("seed", range(48))
+def test_random_workloads_against_oracle(seed):
+    """Seeded random workloads (seed 26: a batch of one empty request), each one layer-step
+    (chained for even seeds, stage by stage for odd ones) checked stage by stage against the
+    oracle: digests, selection (R12 near ties), table, free head, statistics, every pool byte,
+    attention."""
+    spec, s = _random_case(seed)
+    w, st = build(spec, s)
+    say(f"  B={w.B} ctx={list(w.ctx_len)} bs={w.bs} G={w.Hq // w.Hkv} Hkv={w.Hkv} k_mid={list(w.k_mid)} "
+        f"sink/local={w.n_sink}/{w.n_local}")
+    res = full_check(w, st, chained=seed % 2 == 0)
+    say(f"  stats={res['stats']} ties={res['ties']} attn max err {res['attn_err']}")
+
+
 def test_select_overflow_reports_and_empties_request():
     spec, s = W.custom("ovf", [800, 800], Hq=32, Hkv=8, bs=16, k_mid=[5, 30], n_sink=1, n_local=8)
     w, st = build(spec, s, k_max=20)
