@@ -123,3 +123,22 @@ def full_check(w, st, chained=True, run=True):
     out, lse = oracle_attention(w, pool, table, gidx, gcnt)
     err = assert_attention_close(st, out, lse)
     return dict(ties=ties, stats=stats, attn_err=err)
+
+
+def random_case(seed):
+    """A seeded small workload: batch, ragged (and empty) contexts, block size, group size,
+    forced-block counts, budgets from 0 to past the middle, planted or not, free-list order."""
+    rng = np.random.default_rng([seed, 3107])
+    B = int(rng.integers(1, 7))
+    bs = int(rng.choice([16, 32, 64]))
+    Hkv = int(rng.choice([1, 2, 8]))
+    G = int(rng.choice([1, 2, 4, 8, 16]))
+    ctx = [0 if rng.random() < 0.1 else int(rng.integers(1, 24000)) for _ in range(B)]
+    n_max = max(1, max(-(-c // bs) for c in ctx))
+    k_mid = [int(rng.choice([0, int(rng.integers(1, 40)), int(rng.integers(1, n_max + 5))])) for _ in range(B)]
+    n_sink, n_local = int(rng.integers(0, 3)), int(rng.integers(0, 9))
+    spec, s = W.custom(f"rand{seed}", ctx, Hq=G * Hkv, Hkv=Hkv, bs=bs, dtype=str(rng.choice(["bf16", "f16"])),
+                       k_mid=k_mid, n_sink=n_sink, n_local=n_local, resident_frac=float(rng.choice([0.0, 0.1, 0.5])),
+                       heavy_per_req=int(rng.integers(0, 8)), planted=bool(rng.random() < 0.5),
+                       free_order=str(rng.choice(["ascending", "shuffled"])), seed=seed)
+    return spec, s

@@ -13,7 +13,7 @@ from paper_2609_34555_amd import pulse as P
 from paper_2609_34555_amd import workloads as W
 
 from parity import (assert_attention_close, assert_recall_equal, assert_selection_ok, build, full_check,
-                    oracle_attention, oracle_recall, oracle_selection, say)
+                    oracle_attention, oracle_recall, oracle_selection, random_case, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -215,32 +215,13 @@ def test_tied_keys_cut_across_two_tiles():
     assert len(mid) == 151 and copies[0] == 8100 and 8192 <= copies[-1] <= 8300
 
 
-def _random_case(seed):
-    """A seeded small workload: batch, ragged (and empty) contexts, block size, group size,
-    forced-block counts, budgets from 0 to past the middle, planted or not, free-list order."""
-    rng = np.random.default_rng([seed, 3107])
-    B = int(rng.integers(1, 7))
-    bs = int(rng.choice([16, 32, 64]))
-    Hkv = int(rng.choice([1, 2, 8]))
-    G = int(rng.choice([1, 2, 4, 8, 16]))
-    ctx = [0 if rng.random() < 0.1 else int(rng.integers(1, 24000)) for _ in range(B)]
-    n_max = max(1, max(-(-c // bs) for c in ctx))
-    k_mid = [int(rng.choice([0, int(rng.integers(1, 40)), int(rng.integers(1, n_max + 5))])) for _ in range(B)]
-    n_sink, n_local = int(rng.integers(0, 3)), int(rng.integers(0, 9))
-    spec, s = W.custom(f"rand{seed}", ctx, Hq=G * Hkv, Hkv=Hkv, bs=bs, dtype=str(rng.choice(["bf16", "f16"])),
-                       k_mid=k_mid, n_sink=n_sink, n_local=n_local, resident_frac=float(rng.choice([0.0, 0.1, 0.5])),
-                       heavy_per_req=int(rng.integers(0, 8)), planted=bool(rng.random() < 0.5),
-                       free_order=str(rng.choice(["ascending", "shuffled"])), seed=seed)
-    return spec, s
-
-
 @pytest.mark.parametrize("seed", range(48))
 def test_random_workloads_against_oracle(seed):
     """Seeded random workloads (seed 26: a batch of one empty request), each one layer-step
     (chained for even seeds, stage by stage for odd ones) checked stage by stage against the
     oracle: digests, selection (R12 near ties), table, free head, statistics, every pool byte,
     attention."""
-    spec, s = _random_case(seed)
+    spec, s = random_case(seed)
     w, st = build(spec, s)
     say(f"  B={w.B} ctx={list(w.ctx_len)} bs={w.bs} G={w.Hq // w.Hkv} Hkv={w.Hkv} k_mid={list(w.k_mid)} "
         f"sink/local={w.n_sink}/{w.n_local}")
@@ -580,6 +561,25 @@ def test_headwise_selection_and_counts(cid, kw):
     say(f"  solohead: {n_missing} blocks / {n_runs} runs / {nbytes} B;  headwise: {total_units} head-blocks / "
         f"{int(gruns.sum())} runs / {total_units * w.unit_bytes // w.Hkv} B")
     assert total_units > n_missing  # heads disagree on most non-planted blocks
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_workloads_headwise(seed):
+    """Headwise selection (every KV head with its own digests) and its per-head transfer and
+    run counts on the seeded random workloads, against the oracle."""
+    spec, s = random_case(seed)
+    w, st = build(spec, s)
+    sel, cnt, miss, runs = st.headwise()
+    torch.cuda.synchronize()
+    assert st.status() == 0
+    gsel, gcnt = sel.cpu().numpy(), cnt.cpu().numpy()
+    gmiss, gruns = miss.cpu().numpy(), runs.cpu().numpy()
+    osel, ocnt, osc = O.headwise_select(w.kv, w.q, w.blk_off, w.ctx_len, w.Hq, w.Hkv, w.bs, w.d, w.dtype_code,
+                                        w.k_mid, w.n_sink, w.n_local, st.k_max)
+    for h in range(w.Hkv):
+        assert_selection_ok(w, gsel[h], gcnt[h], osel[h], ocnt[h], osc[h])
+        units, nruns = O.missing_counts(gsel[h], gcnt[h], w.table0)
+        assert np.array_equal(gmiss[h], units) and np.array_equal(gruns[h], nruns)
 
 
 # ------------------------------------------------------------------ multi-layer step, two streams

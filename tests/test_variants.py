@@ -66,11 +66,24 @@ def _workload(kw):
 @pytest.mark.gpu
 @pytest.mark.parametrize("name,kw", AVG_CASES, ids=[c[0] for c in AVG_CASES])
 def test_average_selection_matches_oracle(name, kw):
+    spec, s = _workload(kw)
+    _check_average(name, spec, s)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("seed", range(16))
+def test_average_selection_random_workloads(seed):
+    from parity import random_case
+
+    spec, s = random_case(seed)
+    _check_average(f"random {seed}", spec, s)
+
+
+def _check_average(name, spec, s):
     import torch
     from parity import assert_selection_ok, build, say
 
     say(f"\n[gpu] average {name}")
-    spec, s = _workload(kw)
     w, st = build(spec, s)
     scores = torch.zeros(max(w.total_blocks, 1), dtype=torch.float32, device="cuda")
     st.select_average(scores=scores)
