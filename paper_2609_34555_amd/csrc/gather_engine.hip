@@ -119,19 +119,23 @@ __global__ __launch_bounds__(kPublishThreads) void publish_plan_kernel(
     }
 }
 
-// device staging -> pool slots; grid-stride over (block, 16 KiB chunk)
+// device staging -> pool slots; grid-stride over (block, chunk of 4096 * V bytes): 16 KiB
+// chunks (V = 4), or 8 KiB (V = 2) for blocks that are not a multiple of 16 KiB (a block is
+// Hkv * bs * 512 bytes, so it is always a multiple of 8 KiB)
+template <int V>
 __global__ __launch_bounds__(256) void scatter_kernel(const uint8_t* __restrict__ staging,
                                                       const int32_t* __restrict__ slots, int64_t n, int64_t U,
                                                       int32_t n_slots, uint8_t* __restrict__ pool) {
-    const int64_t cpb = U / 16384;
+    constexpr int64_t kChunk = 4096 * V;
+    const int64_t cpb = U / kChunk;
     for (int64_t c = blockIdx.x; c < n * cpb; c += gridDim.x) {
         const int64_t k = c / cpb, part = c - k * cpb;
         const int32_t slot = slots[k];
         if (slot < 0 || slot >= n_slots) continue;
-        const u32x4* src = reinterpret_cast<const u32x4*>(staging + k * U + part * 16384);
-        u32x4* dst = reinterpret_cast<u32x4*>(pool + (int64_t)slot * U + part * 16384);
+        const u32x4* src = reinterpret_cast<const u32x4*>(staging + k * U + part * kChunk);
+        u32x4* dst = reinterpret_cast<u32x4*>(pool + (int64_t)slot * U + part * kChunk);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dst[threadIdx.x + 256 * i] = src[threadIdx.x + 256 * i];
+        for (int i = 0; i < V; ++i) dst[threadIdx.x + 256 * i] = src[threadIdx.x + 256 * i];
     }
 }
 
@@ -260,9 +264,15 @@ struct pulse_gs_engine {
                 st = PULSE_ERR_HIP;
                 break;
             }
-            const int64_t chunks = nb * (int64_t)(U / 16384);
-            hipLaunchKernelGGL(scatter_kernel, dim3((unsigned)std::min<int64_t>(chunks, 1024)), dim3(256), 0, scat,
-                               dev_stage[half], d_slot + b0, nb, (int64_t)U, cur_n_slots, cur_pool);
+            const bool wide = U % 16384 == 0;
+            const int64_t chunks = nb * (int64_t)(U / (wide ? 16384 : 8192));
+            const dim3 sgrid((unsigned)std::min<int64_t>(chunks, 1024));
+            if (wide)
+                hipLaunchKernelGGL(scatter_kernel<4>, sgrid, dim3(256), 0, scat, dev_stage[half], d_slot + b0, nb,
+                                   (int64_t)U, cur_n_slots, cur_pool);
+            else
+                hipLaunchKernelGGL(scatter_kernel<2>, sgrid, dim3(256), 0, scat, dev_stage[half], d_slot + b0, nb,
+                                   (int64_t)U, cur_n_slots, cur_pool);
             if (hipGetLastError() != hipSuccess || hipEventRecord(scat_done[half], scat) != hipSuccess) {
                 st = PULSE_ERR_HIP;
                 break;

@@ -637,6 +637,59 @@ def test_gather_scatter_engine_matches_oracle(cid, kw):
         eng.destroy()
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_workloads_engine_and_release(seed):
+    """On seeded random workloads: the recall through the gather-scatter engine as the oracle
+    does it (table, free head, statistics, every pool byte, then attention); then a chained
+    layer-step that first releases that recall (release_previous) reproduces the oracle's
+    step from the initial state."""
+    spec, s = random_case(seed)
+    w, st = build(spec, s)
+    eng = P.GatherScatterEngine(st.shape, n_workers=2, max_blocks_per_call=max(1, w.B * st.k_max),
+                                staging_blocks=16)
+    try:
+        st.reset()
+        st.select()
+        st.recall_gs(eng)
+        st.attention()
+        torch.cuda.synchronize()
+        assert st.status() == 0
+        full_check(w, st, run=False)
+        st.release(chained=False)
+        torch.cuda.synchronize()
+        assert st.status() == 0 and np.array_equal(st.table_np(), w.table0) and int(st.free_head.item()) == 0
+        st.decode_layer()
+        st.decode_layer(release_previous=True)
+        torch.cuda.synchronize()
+        res = full_check(w, st, run=False)
+        say(f"  stats={res['stats']}")
+    finally:
+        eng.destroy()
+
+
+@pytest.mark.parametrize("Hkv,bs", [(1, 16), (3, 16), (3, 32)])
+def test_gather_scatter_engine_block_sizes(Hkv, bs):
+    """The engine's scatter on blocks of 8 KiB, 24 KiB (not a multiple of its 16 KiB chunks:
+    it copies them in 8 KiB chunks) and 48 KiB: every pool byte, table, free head and
+    statistics as the oracle; attention after completion."""
+    spec, s = W.custom(f"gs_h{Hkv}_bs{bs}", [9000, 2500], Hq=2 * Hkv, Hkv=Hkv, bs=bs, k_mid=[60, 25], n_sink=1,
+                       n_local=4, resident_frac=0.1, heavy_per_req=6)
+    w, st = build(spec, s)
+    assert w.unit_bytes == Hkv * bs * 512
+    eng = P.GatherScatterEngine(st.shape, n_workers=2, max_blocks_per_call=w.B * st.k_max, staging_blocks=16)
+    try:
+        st.reset()
+        st.select()
+        st.recall_gs(eng)
+        st.attention()
+        torch.cuda.synchronize()
+        assert st.status() == 0
+        res = full_check(w, st, run=False)
+        say(f"  unit {w.unit_bytes} B: stats={res['stats']}")
+    finally:
+        eng.destroy()
+
+
 def test_gather_scatter_engine_pool_exhaustion():
     spec, s = W.custom("gsx", [3000, 3000], Hq=32, Hkv=8, bs=16, k_mid=40, n_sink=1, n_local=8,
                        resident_frac=0.05, n_free_override=10)
