@@ -131,8 +131,8 @@ def random_case(seed):
     rng = np.random.default_rng([seed, 3107])
     B = int(rng.integers(1, 7))
     bs = int(rng.choice([16, 32, 64]))
-    Hkv = int(rng.choice([1, 2, 8]))
-    G = int(rng.choice([1, 2, 4, 8, 16]))
+    Hkv = int(rng.choice([1, 2, 3, 8]))  # odd head counts: blocks of 8 KiB multiples that are not 16 KiB ones
+    G = int(rng.choice([1, 2, 3, 4, 8, 16]))
     ctx = [0 if rng.random() < 0.1 else int(rng.integers(1, 24000)) for _ in range(B)]
     n_max = max(1, max(-(-c // bs) for c in ctx))
     k_mid = [int(rng.choice([0, int(rng.integers(1, 40)), int(rng.integers(1, n_max + 5))])) for _ in range(B)]
