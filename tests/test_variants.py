@@ -152,6 +152,23 @@ def test_mam_and_solohead_choice_match_oracle(name, kw):
 
 
 @pytest.mark.gpu
+@pytest.mark.gpu
+@pytest.mark.parametrize("seed", range(8))
+def test_mam_random_workloads(seed):
+    """Eq. 2 per (request, KV head) on seeded random workloads (empty and short requests, odd
+    head counts, bs 16-64) within MAM_TOL of the oracle's token-level masses."""
+    from parity import build, random_case, say
+
+    spec, s = random_case(seed)
+    w, st = build(spec, s)
+    g = st.mam().cpu().numpy()
+    assert st.status() == 0
+    o = _oracle_mam(w)
+    err = float(np.abs(g - o).max()) if g.size else 0.0
+    say(f"\n[gpu] mam random {seed}: B={w.B} Hkv={w.Hkv} bs={w.bs}: max error {err:.2e}")
+    assert err < MAM_TOL
+
+
 def test_mam_reports_missing_block():
     import torch
     from parity import build, say
