@@ -77,3 +77,21 @@ def test_noalloc_release_previous_steps(workloads):
             call(a)
     _assert_same(_state(st), _state(ref))
     full_check(w, st, run=False)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_noalloc_random_workloads(seed):
+    """The static-workspace layer-step on seeded random workloads (odd head counts, empty and
+    ragged requests, bs 16-64): bit-identical to the workspace path and equal to the oracle."""
+    from parity import random_case
+
+    spec, s = random_case(seed)
+    w, ref = build(spec, s)
+    st = H.LayerState(w, ref.host_ptr)
+    ref.reset()
+    P.pulse_decode_layer(ref.layer_args())
+    want = _state(ref)
+    st.reset()
+    P.pulse_decode_layer_noalloc(_noalloc_args(st))
+    _assert_same(_state(st), want)
+    full_check(w, st, run=False)
