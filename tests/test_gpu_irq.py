@@ -76,6 +76,49 @@ def test_irq_mode_matches_chained(setup, mode, use_engine):
     assert (stats["mean_recall_us"] > 0) != use_engine
 
 
+@pytest.fixture(scope="module")
+def random_layers():
+    """Offload layers of different shapes: seeded random workloads (ragged and empty requests,
+    odd head counts, bs 16-64, bf16 / fp16), each with its chained single-stream result."""
+    from parity import build, random_case
+
+    layers, refs = [], []
+    for seed in (1, 3, 6, 11):
+        spec, s = random_case(seed)
+        w, st = build(spec, s)
+        if w.B < 1:
+            continue
+        st.reset()
+        st.decode_layer()
+        torch.cuda.synchronize()
+        refs.append((st.out.clone(), st.lse.clone(), st.table.clone(), st.pool.clone(), st.recall_stats(), st.status()))
+        layers.append(st)
+    return layers, refs
+
+
+@pytest.mark.parametrize("mode", ["semi_sync", "sync", "async", "blocking"])
+def test_irq_random_offload_layers(setup, random_layers, mode):
+    """Every detection mode over offload layers of different shapes (gather-kernel recall):
+    each layer as its chained single-stream step left it, and equal to the oracle."""
+    _, _, normal, sched, _ = setup
+    layers, refs = random_layers
+    say(f"\n[gpu] irq random layers {mode}")
+    for st in layers:
+        st.reset()
+    normal.dev_status.zero_()
+    torch.cuda.synchronize()
+    stats, depth = sched.step([st.layer_args() for st in layers], normal.layers, mode=mode, async_ahead=2)
+    torch.cuda.synchronize()
+    assert stats["offload_layers"] == len(layers)
+    for st, (o, l, t, p, rs, s0) in zip(layers, refs):
+        assert st.status() == s0 == 0
+        assert torch.equal(st.out, o) and torch.equal(st.lse, l)
+        assert torch.equal(st.table, t) and torch.equal(st.pool, p)
+        assert st.recall_stats() == rs
+        full_check(st.w, st, run=False)
+    assert normal.status() == 0
+
+
 @pytest.mark.parametrize("shape", ["b4_ff512", "b37_ff1000", "b20_ff8200_hq9"])
 def test_normal_layers_compute_attention_and_ffn(setup, shape):
     """The normal batch's attention and SwiGLU FFN (the library's MFMA GEMMs) against fp32
