@@ -226,7 +226,8 @@ class LayerState:
         every block is placed in a dense device pool for the calibration."""
         w = self.w
         dev = self.device
-        pool = _dev(w.kv, dev)  # slot b = global block b
+        pool = _dev(w.kv, dev) if w.total_blocks else torch.zeros((1, w.elems_per_block), dtype=torch.int16,
+                                                                 device=dev)  # slot b = global block b
         table = np.full((w.B, w.max_blocks), -1, np.int32)
         for r in range(w.B):
             n = int(w.n_blocks[r])
