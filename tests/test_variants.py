@@ -152,7 +152,6 @@ def test_mam_and_solohead_choice_match_oracle(name, kw):
 
 
 @pytest.mark.gpu
-@pytest.mark.gpu
 @pytest.mark.parametrize("seed", range(8))
 def test_mam_random_workloads(seed):
     """Eq. 2 per (request, KV head) on seeded random workloads (empty and short requests, odd
@@ -169,6 +168,7 @@ def test_mam_random_workloads(seed):
     assert err < MAM_TOL
 
 
+@pytest.mark.gpu
 def test_mam_reports_missing_block():
     import torch
     from parity import build, say
