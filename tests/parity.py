@@ -142,3 +142,21 @@ def random_case(seed):
                        heavy_per_req=int(rng.integers(0, 8)), planted=bool(rng.random() < 0.5),
                        free_order=str(rng.choice(["ascending", "shuffled"])), seed=seed)
     return spec, s
+
+
+def random_case_long(seed):
+    """A seeded workload with long contexts (up to 300K tokens: several 8192-block selection
+    tiles at bs 16) and batches up to 24, budgets up to a few hundred blocks."""
+    rng = np.random.default_rng([seed, 4219])
+    B = int(rng.integers(1, 25))
+    bs = int(rng.choice([16, 32]))
+    Hkv = int(rng.choice([1, 2, 8]))
+    G = int(rng.choice([1, 4, 8]))
+    ctx = [0 if rng.random() < 0.05 else int(rng.integers(1, 300000 if r < 3 else 40000)) for r in range(B)]
+    k_mid = [int(rng.integers(0, 600)) for _ in range(B)]
+    spec, s = W.custom(f"long{seed}", ctx, Hq=G * Hkv, Hkv=Hkv, bs=bs, dtype=str(rng.choice(["bf16", "f16"])),
+                       k_mid=k_mid, n_sink=int(rng.integers(0, 3)), n_local=int(rng.integers(0, 9)),
+                       resident_frac=float(rng.choice([0.0, 0.05, 0.3])), heavy_per_req=int(rng.integers(0, 30)),
+                       planted=bool(rng.random() < 0.5), free_order=str(rng.choice(["ascending", "shuffled"])),
+                       seed=seed)
+    return spec, s

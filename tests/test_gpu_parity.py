@@ -13,7 +13,7 @@ from paper_2609_34555_amd import pulse as P
 from paper_2609_34555_amd import workloads as W
 
 from parity import (assert_attention_close, assert_recall_equal, assert_selection_ok, build, full_check,
-                    oracle_attention, oracle_recall, oracle_selection, random_case, say)
+                    oracle_attention, oracle_recall, oracle_selection, random_case, random_case_long, say)
 
 pytestmark = pytest.mark.gpu
 
@@ -224,6 +224,20 @@ def test_random_workloads_against_oracle(seed):
     spec, s = random_case(seed)
     w, st = build(spec, s)
     say(f"  B={w.B} ctx={list(w.ctx_len)} bs={w.bs} G={w.Hq // w.Hkv} Hkv={w.Hkv} k_mid={list(w.k_mid)} "
+        f"sink/local={w.n_sink}/{w.n_local}")
+    res = full_check(w, st, chained=seed % 2 == 0)
+    say(f"  stats={res['stats']} ties={res['ties']} attn max err {res['attn_err']}")
+
+
+@pytest.mark.parametrize("seed", [1, 6, 7, 19, 24, 39])
+def test_random_long_context_workloads_against_oracle(seed):
+    """Seeded long-context workloads: batches up to 24 requests, the first three up to 300K tokens
+    (up to three 8192-block selection tiles), budgets up to 600 blocks and recalls of up to
+    735 MB, one layer-step (chained for even seeds, stage by stage for odd ones) checked stage
+    by stage against the oracle."""
+    spec, s = random_case_long(seed)
+    w, st = build(spec, s)
+    say(f"  B={w.B} max blocks={int(w.n_blocks.max())} bs={w.bs} G={w.Hq // w.Hkv} Hkv={w.Hkv} "
         f"sink/local={w.n_sink}/{w.n_local}")
     res = full_check(w, st, chained=seed % 2 == 0)
     say(f"  stats={res['stats']} ties={res['ties']} attn max err {res['attn_err']}")
