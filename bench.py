@@ -449,8 +449,9 @@ def timed_steps(torch, P, st, K, warmup):
     events (the roofline kernel) are recorded, on every 4th step: the library attaches them to
     the kernel's launch, but recording events still costs the stream some time between launches.
     Two untimed passes of K steps follow: the scoring kernel's start and the attention's end
-    only (the chain's duration), then all five plus the split-K attention kernel's end (the
-    per-stage split)."""
+    only (the chain's duration), then all five plus, when a merge kernel follows the split-K
+    attention kernel, that kernel's end (the per-stage split; with one workgroup per (request,
+    KV head) the split-K kernel is the whole attention and carries the attention's end itself)."""
     step = st.layer_args(release_previous=True)
     st.reset()  # once, untimed: nothing recalled yet
     for _ in range(warmup):
@@ -459,7 +460,8 @@ def timed_steps(torch, P, st, K, warmup):
     recall = [e.elapsed_ms(2, 3) for e in evs]
     chain_evs, _ = _event_pass(torch, P, st, K, (0, 4))
     layer = [e.elapsed_ms(0, 4) for e in chain_evs]
-    stage_evs, _ = _event_pass(torch, P, st, K, (0, 1, 2, 3, 4), split=True)
+    merge = P.pulse_attention_workgroups(st.shape, st.w.B, st.k_max) > 1
+    stage_evs, _ = _event_pass(torch, P, st, K, (0, 1, 2, 3, 4), split=merge)
     P.pulse_decode_layer(step)  # untimed: leaves this step's recall statistics and tables in place
     torch.cuda.synchronize()
     stage = {"score": [], "select": [], "recall": [], "attention": [], "attention_kernel": [],
@@ -469,13 +471,17 @@ def timed_steps(torch, P, st, K, warmup):
         stage["select"].append(e.elapsed_ms(1, 2))
         stage["recall"].append(e.elapsed_ms(2, 3))
         stage["attention"].append(e.elapsed_ms(3, 4))
-        stage["attention_kernel"].append(e.elapsed_ms(3, 5))
-        stage["attention_combine"].append(e.elapsed_ms(5, 4))
+        if merge:
+            stage["attention_kernel"].append(e.elapsed_ms(3, 5))
+            stage["attention_combine"].append(e.elapsed_ms(5, 4))
+        else:  # no merge kernel: the split-K kernel is the attention
+            stage["attention_kernel"].append(e.elapsed_ms(3, 4))
+            stage["attention_combine"].append(0.0)
         stage["layer"].append(e.elapsed_ms(0, 4))
     for e in evs + chain_evs + stage_evs:
         e.destroy()
     timed = {"recall": statistics.mean(recall), "layer": statistics.mean(layer),
-             "layer_median": statistics.median(layer)}
+             "layer_median": statistics.median(layer), "attention_merge": merge}
     return (wall, timed, {k: statistics.mean(v) for k, v in stage.items()},
             {k: statistics.median(v) for k, v in stage.items()})
 
@@ -554,7 +560,8 @@ def rooflines(w, st, timed, mean, rbytes, peak_measured):
     attn_roof = {"bound": "hbm", "kernel": "attn_splitk_kernel", "achieved": attn, "peak": HBM_GBPS, "unit": "GB/s",
                  "frac": attn / HBM_GBPS, "bytes_per_launch": attn_bytes,
                  "with_combine": {"achieved": attn_call, "frac": attn_call / HBM_GBPS,
-                                  "us": mean["attention"] * 1e3, "combine_us": mean["attention_combine"] * 1e3}}
+                                  "us": mean["attention"] * 1e3, "combine_us": mean["attention_combine"] * 1e3,
+                                  "combine_kernel": timed["attention_merge"]}}
     score_roof = {"bound": "hbm", "kernel": "score_kernel", "achieved": score, "peak": HBM_GBPS, "unit": "GB/s",
                   "frac": score / HBM_GBPS, "bytes_per_launch": digest_bytes}
     return roof, attn_roof, score_roof

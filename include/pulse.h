@@ -355,6 +355,20 @@ PULSE_API pulse_status pulse_sparse_decode_attn(const pulse_shape* shape, const 
                                       float* lse, int32_t* dev_status, void* ws, size_t ws_bytes,
                                       pulse_stream_t stream);
 
+/*
+ * Split-K workgroups per (request, KV head) that pulse_sparse_decode_attn,
+ * and the attention of pulse_decode_layer, launch for a batch of B requests
+ * with at most k_max selected blocks each (the split depends on B, Hkv, k_max
+ * and bs only).  Above 1, a kernel that merges the workgroups' partials
+ * follows the split-K kernel, and pulse_layer_args.attn_split_event marks the
+ * end of the split-K kernel alone.  At 1, one workgroup covers each (request,
+ * KV head) and writes out / lse itself: no merge kernel runs, so a caller that
+ * asks for both attn_split_event and events[4] gets events[4] recorded as a
+ * marker packet after the kernel.  Host function, no device work; 0 for an
+ * unsupported shape, B < 1 or k_max < 1.
+ */
+PULSE_API int32_t pulse_attention_workgroups(const pulse_shape* shape, int32_t B, int32_t k_max);
+
 /* All arguments of one layer-step (pulse_decode_layer).  Field meanings are
  * those of the entry points above. */
 typedef struct {

@@ -78,6 +78,13 @@ size_t pulse_workspace_bytes(const pulse_shape* shape, int32_t B, int32_t k_max,
     return ws_layout(*shape, B, k_max, total_blocks).total;
 }
 
+int32_t pulse_attention_workgroups(const pulse_shape* shape, int32_t B, int32_t k_max) {
+    if (!shape_supported(shape) || B < 1 || k_max < 1) return 0;
+    const AttnPlan p = attn_plan(B, shape->num_kv_heads, k_max, shape->block_size);
+    const int W = attn_waves(shape->num_q_heads / shape->num_kv_heads);
+    return (p.n_split + W - 1) / W;
+}
+
 pulse_status pulse_build_digests(const pulse_shape* shape, const void* kv, const int64_t* blk_off,
                                  const int32_t* ctx_len, int32_t B, int64_t total_blocks, int32_t kv_head,
                                  void* digests, int32_t* dev_status, pulse_stream_t stream) {

@@ -38,7 +38,7 @@ EXPORTED = (
     "pulse_gs_recall_poll", "pulse_gs_recall_wait", "pulse_gs_last_timing", "pulse_overlap_depth",
     "pulse_ioaa_plan", "pulse_average_workspace_bytes", "pulse_select_average", "pulse_mam_workspace_bytes",
     "pulse_mam", "pulse_pick_solo_heads", "pulse_irq_create", "pulse_irq_destroy", "pulse_irq_step",
-    "pulse_probe_hbm_read", "pulse_probe_hbm_sink_bytes", "pulse_release_recalled",
+    "pulse_probe_hbm_read", "pulse_probe_hbm_sink_bytes", "pulse_release_recalled", "pulse_attention_workgroups",
 )
 
 
@@ -141,6 +141,7 @@ def signatures():
         "pulse_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "pulse_block_bytes": (SZ, [SP]),
         "pulse_workspace_bytes": (SZ, [SP, I32, I32, I64]),
+        "pulse_attention_workgroups": (I32, [SP, I32, I32]),
         "pulse_build_digests": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, _P, _P]),
         "pulse_select_solohead": (ctypes.c_int, [SP, _P, _P, _P, I32, I64, I32, _P, I32, I32, I32, _P, _P, _P,
                                                  _P, _P, SZ, _P]),
@@ -232,6 +233,11 @@ def pulse_block_bytes(shape: pulse_shape) -> int:
 
 def pulse_workspace_bytes(shape: pulse_shape, B: int, k_max: int, total_blocks: int) -> int:
     return lib().pulse_workspace_bytes(ctypes.byref(shape), B, k_max, total_blocks)
+
+
+def pulse_attention_workgroups(shape: pulse_shape, B: int, k_max: int) -> int:
+    """Split-K workgroups per (request, KV head) of the attention; above 1 a merge kernel follows."""
+    return lib().pulse_attention_workgroups(ctypes.byref(shape), B, k_max)
 
 
 def pulse_build_digests(shape, kv, blk_off, ctx_len, B, total_blocks, kv_head, digests, dev_status=None,

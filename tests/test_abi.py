@@ -75,6 +75,19 @@ def test_block_and_workspace_sizes():
     assert P.pulse_workspace_bytes(shape(), -1, 128, 10) == 0
 
 
+def test_attention_workgroups():
+    """Split-K workgroups per (request, KV head): one (no merge kernel) where 8 waves cover a
+    selection at the ~2048-wave sizing, several otherwise; 0 for invalid arguments."""
+    assert P.pulse_attention_workgroups(shape(), 32, 256) == 1  # 32 x 8 units, 8 splits of 32 blocks
+    assert P.pulse_attention_workgroups(shape(), 8, 128) == 4  # 64 units, 32 splits of 4 blocks
+    assert P.pulse_attention_workgroups(shape(num_q_heads=64, block_size=32), 4, 256) == 8
+    assert P.pulse_attention_workgroups(shape(dtype=P.PULSE_F16), 1, 25) == 1  # 7 splits, one workgroup
+    assert P.pulse_attention_workgroups(shape(num_q_heads=8 * 12), 8, 128) == 8  # G 12: 4-wave workgroups
+    assert P.pulse_attention_workgroups(shape(), 0, 128) == 0
+    assert P.pulse_attention_workgroups(shape(), 8, 0) == 0
+    assert P.pulse_attention_workgroups(shape(head_dim=64), 8, 128) == 0
+
+
 FAKE = 0x1000  # never dereferenced: every call below fails validation first
 
 
