@@ -543,6 +543,59 @@ def attention_warm_cold(torch, st, attn_bytes, reps=10):
     return res
 
 
+def selection_variants(torch, P, st, w, reps=10):
+    """Scoring + selection by the three strategies of Sec. 4.4.1 on this workload, each call
+    alone: SoloHead (one KV head's digests), Average (every KV head scores, the scores are
+    averaged, one selection) and headwise (every KV head selects for itself, with its transfer
+    and run counts against the block table).  The digests of every head are built first
+    (untimed); outputs go to buffers of their own, so the step's state is untouched.  Events
+    recorded around each launch on the current stream (each interval carries a marker's cost,
+    the same for all three); mean over `reps` calls after two warm-ups."""
+    hd = st.all_head_digests()
+    dev = st.device
+    H, B, k, nt = w.Hkv, w.B, st.k_max, w.total_blocks
+    sel = torch.full((H, B, k), -1, dtype=torch.int32, device=dev)
+    cnt = torch.zeros((H, B), dtype=torch.int32, device=dev)
+    miss, runs = torch.zeros_like(cnt), torch.zeros_like(cnt)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    nb = {"solohead": P.pulse_workspace_bytes(st.shape, B, k, nt),
+          "average": P.pulse_average_workspace_bytes(st.shape, B, k, nt),
+          "headwise": P.pulse_headwise_workspace_bytes(st.shape, B, k, nt)}
+    ws = torch.zeros(max(max(nb.values()), 1), dtype=torch.uint8, device=dev)
+    calls = {
+        "solohead": lambda: P.pulse_select_solohead(st.shape, st.q, st.digests, st.blk_off, B, nt, w.solo_kv_head,
+                                                    st.k_mid, w.n_sink, w.n_local, k, sel[0], cnt[0], None, status,
+                                                    ws, nb["solohead"]),
+        "average": lambda: P.pulse_select_average(st.shape, st.q, hd, st.blk_off, B, nt, st.k_mid, w.n_sink,
+                                                  w.n_local, k, sel[0], cnt[0], None, status, ws, nb["average"]),
+        "headwise": lambda: P.pulse_select_headwise(st.shape, st.q, hd, st.blk_off, B, nt, st.k_mid, w.n_sink,
+                                                    w.n_local, k, st.table, w.max_blocks, w.n_slots, sel, cnt, miss,
+                                                    runs, status, ws, nb["headwise"]),
+    }
+    out = {}
+    for name, fn in calls.items():
+        for _ in range(2):
+            fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(20_000_000)  # keeps the GPU busy while the launches below are enqueued
+        for e0, e1 in evs:
+            e0.record()
+            fn()
+            e1.record()
+        torch.cuda.synchronize()
+        out[name + "_us"] = statistics.mean(e0.elapsed_time(e1) for e0, e1 in evs) * 1e3
+    if int(status.item()) != 0:
+        raise RuntimeError(f"device status {int(status.item())} in the selection variants")
+    per_head = int(sum(max(0, n - w.n_sink - w.n_local) for n in w.n_blocks.tolist())) * 2 * w.d * 2
+    out["digest_bytes_read"] = {"solohead": per_head, "average": per_head * H, "headwise": per_head * H}
+    out["digest_bytes_resident"] = {"solohead": nt * 2 * w.d * 2, "every_head": nt * 2 * w.d * 2 * H}
+    del hd, ws
+    st.head_digests = None
+    torch.cuda.empty_cache()
+    return out
+
+
 def rooflines(w, st, timed, mean, rbytes, peak_measured):
     """The recall's rate from the timed region's events; attention and score from the
     all-stage pass."""
@@ -643,6 +696,7 @@ def bench_layer(cid, args, torch, P, H, W, compact=False):
             r["frac_of_measured"] = r["achieved"] / r["peak_measured"]
         extras["hbm_read_1GiB_GBps"] = hbm_probe(torch, P, 1 << 30)
         attn_roof["isolated"] = attention_warm_cold(torch, st, attn_roof["bytes_per_launch"])
+        extras["selection_variants"] = selection_variants(torch, P, st, w)
     attach_traffic(cid, roof, attn_roof, score_roof)
     line = base_line(cid, K, args.warmup)
     line.update({
