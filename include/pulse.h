@@ -547,8 +547,9 @@ PULSE_API pulse_status pulse_irq_destroy(pulse_irq* irq);
  * at each normal layer boundary as `mode` says (ASYNC: at most async_ahead
  * normal layers queued); then the offload attention for layer m is enqueued
  * (after a stream wait on the recall) and layer m + 1 follows.  With `engine`
- * (a pulse_gs_engine for the offload layers' shape) the recall goes through
- * the gather-scatter engine instead, submitted on the compute stream, and its
+ * (a pulse_gs_engine for the offload layers' shape; an offload layer of
+ * another shape -> PULSE_ERR_INVALID_ARG before any work) the recall goes
+ * through the gather-scatter engine instead, submitted on the compute stream, and its
  * host-side completion is the flag; the gather kernel path stalls concurrent
  * kernels on MI355X while it reads host memory, the engine's DMA does not.
  * Results of the offload batch are those of pulse_decode_layer on each layer

@@ -313,6 +313,11 @@ struct pulse_gs_engine {
     }
 };
 
+bool pulse::gs_engine_serves(const pulse_gs_engine* e, const pulse_shape& s) {
+    return e->shape.num_q_heads == s.num_q_heads && e->shape.num_kv_heads == s.num_kv_heads &&
+           e->shape.head_dim == s.head_dim && e->shape.block_size == s.block_size && e->shape.dtype == s.dtype;
+}
+
 extern "C" {
 
 pulse_status pulse_gs_engine_create(const pulse_shape* shape, int32_t n_workers, int64_t max_blocks_per_call,

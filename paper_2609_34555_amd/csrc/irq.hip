@@ -430,6 +430,8 @@ pulse_status pulse_irq_step(pulse_irq* irq, const pulse_layer_args* offload, int
         pulse_status st = check_layer_args(&offload[m]);
         if (st != PULSE_OK) return st;
         PULSE_REQUIRE(offload[m].B >= 1, PULSE_ERR_INVALID_ARG);
+        // the engine moves blocks of the shape it was made for
+        PULSE_REQUIRE(!engine || gs_engine_serves(engine, offload[m].shape), PULSE_ERR_INVALID_ARG);
     }
     for (int32_t l = 0; l < n_normal_layers; ++l) {
         pulse_status st = check_normal(&normal[l]);

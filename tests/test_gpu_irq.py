@@ -119,6 +119,55 @@ def test_irq_random_offload_layers(setup, random_layers, mode):
     assert normal.status() == 0
 
 
+SAME_SHAPE_SEEDS = {"hq48_hkv3_bs16_f16": (2036, 2076, 2156, 2197),  # 24 KiB blocks: 8 KiB scatter chunks
+                    "hq64_hkv8_bs32_bf16": (2002, 2029, 2077, 2132)}  # 128 KiB blocks, G 8
+
+
+@pytest.fixture(scope="module", params=sorted(SAME_SHAPE_SEEDS))
+def same_shape_layers(request):
+    """Four seeded random offload layers of one shape (ragged and empty contexts, budgets, free
+    orders differ), each with its chained single-stream result, and an engine for that shape."""
+    from parity import build, random_case
+
+    layers, refs = [], []
+    for seed in SAME_SHAPE_SEEDS[request.param]:
+        spec, s = random_case(seed)
+        w, st = build(spec, s)
+        st.reset()
+        st.decode_layer()
+        torch.cuda.synchronize()
+        refs.append((st.out.clone(), st.lse.clone(), st.table.clone(), st.pool.clone(), st.recall_stats(), st.status()))
+        layers.append(st)
+    assert len({(st.w.Hq, st.w.Hkv, st.w.bs, st.w.dtype_code) for st in layers}) == 1
+    engine = P.GatherScatterEngine(layers[0].shape, 2, max(st.w.B * st.k_max for st in layers), 16)
+    yield layers, refs, engine
+    engine.destroy()
+
+
+@pytest.mark.parametrize("mode", ["semi_sync", "sync", "async", "blocking"])
+def test_irq_engine_random_offload_layers(setup, same_shape_layers, mode):
+    """Every detection mode with the paper's recall engine over random offload layers of one
+    shape: each layer as its chained single-stream step left it, and equal to the oracle."""
+    _, _, normal, sched, _ = setup
+    layers, refs, engine = same_shape_layers
+    say(f"\n[gpu] irq engine random layers {mode}")
+    for st in layers:
+        st.reset()
+    normal.dev_status.zero_()
+    torch.cuda.synchronize()
+    stats, depth = sched.step([st.layer_args() for st in layers], normal.layers, mode=mode, async_ahead=2,
+                              engine=engine)
+    torch.cuda.synchronize()
+    assert stats["offload_layers"] == len(layers)
+    for st, (o, l, t, p, rs, s0) in zip(layers, refs):
+        assert st.status() == s0 == 0
+        assert torch.equal(st.out, o) and torch.equal(st.lse, l)
+        assert torch.equal(st.table, t) and torch.equal(st.pool, p)
+        assert st.recall_stats() == rs
+        full_check(st.w, st, run=False)
+    assert normal.status() == 0
+
+
 @pytest.mark.parametrize("shape", ["b4_ff512", "b37_ff1000", "b20_ff8200_hq9"])
 def test_normal_layers_compute_attention_and_ffn(setup, shape):
     """The normal batch's attention and SwiGLU FFN (the library's MFMA GEMMs) against fp32
@@ -178,3 +227,11 @@ def test_irq_rejects_bad_arguments(setup):
         assert e.value.status == P.PULSE_ERR_INVALID_ARG
     finally:
         L.d_ff, L.w_down = d_ff, w_down
+    # an engine made for another shape would move blocks of the wrong size: rejected
+    other = P.GatherScatterEngine(P.make_shape(16, 4, 128, 16, P.PULSE_BF16), 2, 64, 16)
+    try:
+        with pytest.raises(P.PulseError) as e:
+            sched.step([ml.layers[0].layer_args()], normal.layers, engine=other)
+        assert e.value.status == P.PULSE_ERR_INVALID_ARG
+    finally:
+        other.destroy()
