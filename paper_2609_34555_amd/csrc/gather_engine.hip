@@ -313,10 +313,13 @@ struct pulse_gs_engine {
     }
 };
 
-bool pulse::gs_engine_serves(const pulse_gs_engine* e, const pulse_shape& s) {
+namespace pulse {
+// Whether an engine was created for shape `s` (pulse_irq_step checks every offload layer).
+bool gs_engine_serves(const pulse_gs_engine* e, const pulse_shape& s) {
     return e->shape.num_q_heads == s.num_q_heads && e->shape.num_kv_heads == s.num_kv_heads &&
            e->shape.head_dim == s.head_dim && e->shape.block_size == s.block_size && e->shape.dtype == s.dtype;
 }
+}  // namespace pulse
 
 extern "C" {
 

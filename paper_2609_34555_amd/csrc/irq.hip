@@ -325,6 +325,12 @@ static unsigned grid_for(int64_t n) {
 
 }  // namespace pulse
 
+namespace pulse {
+// gather_engine.hip: whether an engine was created for shape `s` (its block size and
+// staging are that shape's)
+bool gs_engine_serves(const pulse_gs_engine* e, const pulse_shape& s);
+}  // namespace pulse
+
 using namespace pulse;
 
 struct pulse_irq {

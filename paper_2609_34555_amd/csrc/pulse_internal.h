@@ -256,8 +256,4 @@ int32_t probe_hbm_sink_words();
 
 hipError_t launch_probe_copy(const void* src, void* dst, size_t bytes, hipStream_t st);
 
-// Whether a gather-scatter engine was created for `s` (its block size and staging
-// are that shape's).
-bool gs_engine_serves(const pulse_gs_engine* e, const pulse_shape& s);
-
 }  // namespace pulse
