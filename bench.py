@@ -812,6 +812,9 @@ def bench_multilayer(args, torch, P, H, W, compact=False):
         st.head_digests = None
     w0 = ml.layers[0].w
     U = w0.unit_bytes
+    extras = {}
+    if args.profile and not compact:
+        extras["calibration"] = calibration_copies(torch, P)
     line = base_line(4, K, args.warmup)
     sampled_bytes = sum(per_layer[i][2] for i in sampled)
     recall_GBps = sampled_bytes / (sampled_ms * 1e-3) / 1e9
@@ -831,9 +834,15 @@ def bench_multilayer(args, torch, P, H, W, compact=False):
                      "peak": PCIE5_X16_GBPS, "unit": "GB/s", "frac": recall_GBps / PCIE5_X16_GBPS,
                      "bytes_per_launch": rbytes / len(ml.layers), "traffic": None,
                      "timed_layers": sampled},
+        "extras": extras,
         "attention_ms_per_step": attn_ms,
         "setup_s": {"generate_and_upload": gen_s},
     })
+    # every pass recalls each layer once, so the mean per-launch counter reading is the mean
+    # over layers, the same average as bytes_per_launch
+    rec = counter_traffic("recall_copy_kernel", 4)
+    line["roofline"]["traffic"] = (rec or {}).get("total")
+    line["roofline"]["traffic_split"] = rec
     if not (args.no_cpu_baseline or args.profile or compact):
         line["cpu_baseline"] = cpu_baseline(w0, args.cpu_seconds, "layer 0 of the 32-layer step")
     del ml
